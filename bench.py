@@ -1,0 +1,189 @@
+"""Benchmark of one MAP-Elites generation step on one MI355X.
+
+A step is one qd_generation() call: uniform selection, Iso+LineDD variation,
+batched evaluation, descriptor -> cell and insertion, over one batch of N_B
+offspring, with the archive resident in HBM.  The default workload is the
+Rastrigin-projection configuration at N_B = 65536 (n = 1000, CVT of 10^4
+cells).  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                  [--no-cpu-baseline] [--cpu-generations G]
+
+Throughput `value` = N_B * K / (wall time of the K timed steps), bracketed by
+device synchronisation.  The paper's eval/s (mean over steps of N_B / t_n) is
+reported beside it from per-step HIP events.  The roofline object is for the
+dominant kernel, whose per-launch duration comes from HIP events that the
+library records around every launch on its stream during the timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "offspring evaluated+inserted/sec at 1 MI355X; % of peak HBM BW"
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+FP32_PEAK_TFLOPS = 157.3     # MI355X fp32 vector (dual-issue / packed) peak
+
+
+def log(msg: str):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w: dict, n: int) -> dict:
+    """Bytes each offspring must move at least (byte model).
+
+    vary_eval: both parent rows (8n), objective and descriptor (4 + 4D), two
+    parent indices (8), won flag (1).  Whole generation adds the cell index
+    write and read (8), the key (8) and the winners' rows, which the
+    benchmark reports separately through the measured insertion count."""
+    D = w["D"]
+    vary = 8 * n + 4 + 4 * D + 8 + 1
+    gen = 8 * n + 4 * (1 + D) + 4 + 8
+    return dict(vary_eval=vary, generation=gen, winner_row=4 * n + 4 + 4 * D)
+
+
+def mlp_flops(w: dict) -> float:
+    """fp32 flops of one rollout (2 per multiply-add), excluding tanh."""
+    o, h, a, T = w["obs"], w["hid"], w["act"], w["T"]
+    macs = h * o + h * h + a * h + o * o + o * a + a
+    return 2.0 * macs * T
+
+
+def cpu_baseline(w: dict, gens: int) -> dict:
+    """The oracle, single-threaded, on a bounded sample of the same workload."""
+    from oracle import oracle as O
+    o = O.Oracle(w)
+    t0 = time.perf_counter()
+    if w["task"] == 3:
+        # policies: a sample of individuals of the first batch is the unit
+        import numpy as np
+        o.setup()
+        count = gens
+        for j in range(count):
+            o.offspring(0, j)
+        dt = time.perf_counter() - t0
+        return dict(value=count / dt, unit="offspring/s", cores=1, kind="oracle",
+                    sample=f"{count} rollouts (T={w['T']}) of the first batch, one thread")
+    o.init()
+    t_init = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    for g in range(1, gens + 1):
+        o.generation(g)
+    dt = time.perf_counter() - t1
+    return dict(value=gens * w["batch"] / dt, unit="offspring/s", cores=1, kind="oracle",
+                sample=f"{gens} full generations of N_B={w['batch']} after the first batch "
+                       f"({t_init:.1f} s, untimed), one thread")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="rastrigin_proj_cvt_b65536")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-generations", type=int, default=2)
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the method shards as described in DESIGN.md, but only one GPU is used here)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2202_01258_amd import qd, workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    w = W.workload(args.workload)
+    n = W.genotype_len(w)
+    nb = w["batch"]
+    log(f"bench: workload {args.workload} N_B={nb} n={n} C={w['C']}; setting up")
+    a = qd.Archive(w, device="cuda:0")
+    stream = a.stream
+    stream.synchronize()
+    g = 1
+    for _ in range(args.warmup):
+        a.generation(g)
+        g += 1
+    stream.synchronize()
+    log(f"bench: {args.warmup} warmup steps done; timing {args.steps} steps")
+
+    if not args.no_kernel_timing:
+        a.set_kernel_timing(True)
+        a.kernel_times()          # clear
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for k in range(args.steps):
+        a.generation(g)
+        g += 1
+        ev[k + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall = t1 - t0
+    step_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
+    ktimes = a.kernel_times() if not args.no_kernel_timing else {}
+    a.set_kernel_timing(False)
+    st = a.stats()
+    log(f"bench: timed region {wall * 1e3:.2f} ms; coverage {st['num_occupied']} cells")
+
+    value = nb * args.steps / wall
+    paper_evals = sum(nb / (t / 1e3) for t in step_ms) / len(step_ms)
+    ms_per_step = wall * 1e3 / args.steps
+    bytes_model = algorithmic_bytes(w, n)
+    line = {
+        "metric": METRIC, "value": value, "unit": "offspring/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded Philox streams; no dataset)",
+        "config": {"workload": args.workload, "task": ["rastrigin", "sphere",
+                   "rastrigin_projection", "mlp_policy"][w["task"]],
+                   "batch": nb, "genotype_dim": n, "cells": w["C"],
+                   "tessellation": "grid" if w["tess"] == 0 else "cvt",
+                   "episode_len": w["T"] if w["task"] == 3 else None, "seed": w["seed"]},
+        "paper_eval_per_s": paper_evals,
+        "median_step_ms": sorted(step_ms)[len(step_ms) // 2],
+        "archive": {"filled_cells": st["num_occupied"], "qd_score": st["qd_score"],
+                    "best": st["best"]},
+    }
+    gen_bytes = bytes_model["generation"] * nb
+    line["generation_hbm_frac"] = gen_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9)
+    if ktimes:
+        line["kernel_ms_per_step"] = {k: (v[0] / v[1] if v[1] else 0.0)
+                                      for k, v in ktimes.items() if v[1]}
+        if w["task"] == 3:
+            ms, cnt = ktimes["rollout"]
+            avg = ms / cnt
+            flops = mlp_flops(w) * nb
+            ach = flops / (avg * 1e-3) / 1e12
+            line["roofline"] = {"kernel": "k_rollout", "bound": "alu", "achieved": ach,
+                                "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                "frac": ach / FP32_PEAK_TFLOPS, "traffic": None}
+        else:
+            ms, cnt = ktimes["vary_eval"]
+            avg = ms / cnt
+            ach = bytes_model["vary_eval"] * nb / (avg * 1e-3) / 1e9
+            line["roofline"] = {"kernel": "k_vary_eval", "bound": "hbm", "achieved": ach,
+                                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                                "kernel_avg_us": avg * 1e3}
+    if not args.no_cpu_baseline:
+        log("bench: CPU baseline (oracle, one thread)")
+        cb_w = dict(w)
+        line["cpu_baseline"] = cpu_baseline(cb_w, args.cpu_generations if w["task"] != 3 else 4)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,175 @@
+/*
+ * qd.h -- C ABI of the MI355X (gfx950) MAP-Elites generation library, libqd.so.
+ *
+ * One call of qd_generation() runs one iteration of MAP-Elites after the first
+ * (Algorithm 1 of "Accelerated Quality-Diversity through Massive Parallelism",
+ * arXiv 2202.01258): uniform selection of parents from the filled cells
+ * (Appendix A.2), Iso+LineDD variation (Algorithm 2, Appendix A.2), batched
+ * evaluation of the N_B offspring (Appendix A.3 and B.2), descriptor to cell
+ * (Appendix A.1) and per-cell insertion that keeps the better solution
+ * (Algorithm 1, Appendix A.4).  All of it runs in HIP kernels on the caller's
+ * stream; no call here returns control to the host between those steps.
+ *
+ * Conventions for every entry point:
+ *   - Plain C types only.  `stream` is a hipStream_t passed as void* (NULL =
+ *     the default stream).  Device pointers are plain void*.
+ *   - Every call returns a qd_status; nothing throws across the ABI.
+ *   - The caller owns all device memory: one workspace of
+ *     qd_layout.workspace_bytes bytes, 256-byte aligned, sized by
+ *     qd_layout_query().  The library never allocates or frees device memory.
+ *     The library owns only the small host handle made by qd_archive_init().
+ *   - A handle is not thread-safe; separate handles (with separate
+ *     workspaces) are independent.  Calls on one handle must be ordered on one
+ *     stream, or the caller orders the streams.
+ *   - Numbers are fp32 except insertion keys (u64) and the statistics (fp64).
+ */
+#ifndef QD_H
+#define QD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QD_ABI_VERSION 1u
+
+typedef enum {
+  QD_OK = 0,
+  QD_ERR_INVALID_ARG = 1,          /* bad config field, null pointer, bad g     */
+  QD_ERR_WORKSPACE_TOO_SMALL = 2,  /* workspace shorter than the layout needs   */
+  QD_ERR_EMPTY_ARCHIVE = 3,        /* selection found no filled cell            */
+  QD_ERR_UNSUPPORTED = 4,          /* valid but not built (e.g. hidden width)   */
+  QD_ERR_HIP = 5                   /* a HIP runtime or launch error             */
+} qd_status;
+
+/* Tasks (Appendix B.2 test functions; a synthetic policy rollout). */
+enum { QD_TASK_RASTRIGIN = 0, QD_TASK_SPHERE = 1, QD_TASK_RASTRIGIN_PROJ = 2,
+       QD_TASK_MLP_SYNTH = 3 };
+/* Tessellations: regular grid, or nearest of num_cells centroids (CVT). */
+enum { QD_TESS_GRID = 0, QD_TESS_CVT = 1 };
+
+typedef struct {
+  uint32_t abi_version;   /* QD_ABI_VERSION                                       */
+  int32_t task;           /* QD_TASK_*                                            */
+  int32_t tess;           /* QD_TESS_*                                            */
+  int32_t genotype_dim;   /* n for the test functions; must be 0 for MLP          */
+  int32_t batch_size;     /* N_B >= 1                                             */
+  int32_t desc_dim;       /* D: 2 for the test functions, 4 for MLP               */
+  int32_t grid_shape[4];  /* grid: bins per dimension; prod == num_cells          */
+  int32_t num_cells;      /* C                                                    */
+  float desc_lo[4];       /* descriptor box; the CVT maps it onto [0,1]^D and    */
+  float desc_hi[4];       /*   the test-function descriptors are clipped to it    */
+  float iso_sigma;        /* sigma_1 of Algorithm 2                               */
+  float line_sigma;       /* sigma_2 of Algorithm 2                               */
+  float init_lo, init_hi; /* first batch of the test functions: U[lo, hi)        */
+  int32_t mlp_obs;        /* policy: observation size (27)                        */
+  int32_t mlp_hidden;     /*         hidden width (64 or 128)                     */
+  int32_t mlp_act;        /*         actions (8)                                  */
+  int32_t episode_len;    /*         rollout steps T                              */
+  int32_t keep_offspring; /* 1: also store every offspring genotype (tests)       */
+  uint64_t seed;          /* key of every Philox4x32-10 stream                    */
+} qd_config;
+
+/* Workspace buffers, in layout order.  Offsets/sizes are in bytes. */
+enum {
+  QD_BUF_ARCHIVE_KEY = 0,  /* u64 [C]   0 = empty; else (order(f) << 32) | 0xFFFFFFFF */
+  QD_BUF_ARCHIVE_FIT,      /* f32 [C]   objective of the elite (NaN when empty)       */
+  QD_BUF_ARCHIVE_DESC,     /* f32 [C][D]                                              */
+  QD_BUF_ARCHIVE_SLOT,     /* u32 [C]   which genotype bank (0/1) holds the elite     */
+  QD_BUF_ARCHIVE_GENO,     /* f32 [2][C][row_stride] two genotype banks               */
+  QD_BUF_CENTROIDS,        /* f32 [C][D] CVT centroids                                */
+  QD_BUF_BUCKET_START,     /* i32 [num_buckets + 1] CVT bucket offsets                */
+  QD_BUF_BUCKET_ITEMS,     /* f32x4 + i32: bucketed centroid copies and indices       */
+  QD_BUF_ENV,              /* f32: A [obs][obs], B [obs][act], s0 [obs]               */
+  QD_BUF_OCC_LIST,         /* i32 [C]   filled cells, ascending                       */
+  QD_BUF_COUNTERS,         /* i32 [64]  [0] = number of filled cells, [1] = flags     */
+  QD_BUF_OFF_PARENTS,      /* i32 [N_B][2] parent cells of the last batch            */
+  QD_BUF_OFF_FIT,          /* f32 [N_B]                                               */
+  QD_BUF_OFF_DESC,         /* f32 [N_B][D]                                            */
+  QD_BUF_OFF_CELL,         /* i32 [N_B] cell, -1 = invalid (never inserted)          */
+  QD_BUF_OFF_WON,          /* u8  [N_B] 1 = holds its cell after the batch           */
+  QD_BUF_OFF_GENO,         /* f32 [N_B][row_stride] (keep_offspring only)            */
+  QD_BUF_STATS,            /* f64 [8]   device-side statistics                        */
+  QD_NUM_BUFFERS
+};
+
+typedef struct {
+  uint64_t workspace_bytes;
+  uint64_t offset[QD_NUM_BUFFERS];
+  uint64_t bytes[QD_NUM_BUFFERS];
+  int32_t genotype_dim;    /* n (derived for MLP: h*obs + h + h*h + h + act*h + act) */
+  int32_t row_stride;      /* floats between genotype rows (multiple of 64)          */
+  int32_t bucket_res;      /* CVT buckets per dimension (0 for the grid)             */
+  int32_t num_buckets;
+} qd_layout;
+
+typedef struct {
+  double qd_score;         /* sum over filled cells of (f + qd_offset), Eq. 1        */
+  double coverage;         /* filled cells / C                                       */
+  float best_fitness;      /* max f over filled cells (NaN when empty)               */
+  int32_t num_occupied;
+  uint32_t flags;          /* bit 0: a generation found the archive empty            */
+  int32_t reserved;
+} qd_stats;
+
+typedef struct qd_archive qd_archive;
+
+/* Kernels whose durations qd_kernel_times() reports. */
+enum { QD_K_VARY_EVAL = 0, QD_K_ROLLOUT, QD_K_CELL_INSERT, QD_K_REGEN, QD_K_FINALIZE,
+       QD_K_SETUP, QD_NUM_KERNELS };
+
+/* Validates *cfg and fills *out with the workspace layout.  Host only; no GPU
+ * work.  QD_ERR_INVALID_ARG for an inconsistent config (task/tessellation/D
+ * mismatch, grid product != num_cells, n <= 0, N_B <= 0, genotype_dim != 0 for
+ * MLP, sizes overflowing 64 bits), QD_ERR_UNSUPPORTED for a valid config this
+ * build has no kernel for. */
+qd_status qd_layout_query(const qd_config* cfg, qd_layout* out);
+
+/* Creates an archive in the caller's workspace and enqueues its first
+ * iteration on `stream` (Algorithm 1, random solutions): CVT centroids and the
+ * synthetic environment from their Philox streams, an empty archive, N_B
+ * random genotypes evaluated and inserted.  Asynchronous: returns once the
+ * work is enqueued.  *out receives a host handle owned by the library (free it
+ * with qd_archive_destroy).  The workspace must stay valid until then. */
+qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t workspace_bytes,
+                          void* stream, qd_archive** out);
+
+/* Enqueues generation gen_index (>= 1) on `stream`: select, vary, evaluate,
+ * map to cells, insert.  gen_index keys every Philox stream of the generation,
+ * so replaying a generation from the same archive state reproduces it exactly.
+ * Asynchronous: no host synchronisation.  The per-offspring buffers
+ * (QD_BUF_OFF_*) hold this batch until the next call.  An archive found empty
+ * on the device sets flag bit 0 (reported by qd_archive_stats) and inserts
+ * nothing. */
+qd_status qd_generation(qd_archive* h, uint32_t gen_index, void* stream);
+
+/* QD-score (Eq. 1) with each filled cell's objective shifted by qd_offset,
+ * coverage and best objective (Appendix B.1), computed on the device and
+ * copied into *out.  Synchronises `stream` (the only call that does). */
+qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_stats* out);
+
+/* The layout the handle was created with. */
+qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
+
+/* Turns per-kernel timing on or off.  When on, every launch is bracketed by
+ * HIP events on the launch stream. */
+qd_status qd_set_kernel_timing(qd_archive* h, int32_t enable);
+
+/* Waits for the recorded events and returns, per QD_K_* kernel, the summed
+ * duration in ms and the number of launches since the last call; then clears
+ * them.  ms and counts must hold QD_NUM_KERNELS entries. */
+qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts);
+
+/* Frees the host handle (not the workspace).  NULL is accepted. */
+qd_status qd_archive_destroy(qd_archive* h);
+
+/* Static description of a status; for QD_ERR_HIP, of the last HIP error the
+ * library saw on this thread. */
+const char* qd_status_str(qd_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,195 @@
+// qd_device.hpp -- device-side arithmetic of the generation kernels (gfx950).
+//
+// Counter-based random numbers, the Gaussian sampler and the fp32
+// transcendental functions the kernels use.  Every function here is evaluated
+// with explicit fused multiply-adds in a fixed order and the library is built
+// with -ffp-contract=off, so each result is a fixed function of its inputs,
+// independent of launch shape or scheduling.  That makes a generation
+// reproducible bit for bit, which the insertion step needs: which elite keeps
+// a cell is decided by comparing fp32 objectives.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qd {
+
+// ---------------------------------------------------------------------------
+// Philox4x32 with 10 rounds (Salmon et al., SC'11).  Counter words:
+// (item, individual, generation, stream tag); key = the 64-bit seed.
+// ---------------------------------------------------------------------------
+enum : uint32_t { kTagInit = 0, kTagSelect = 1, kTagIso = 2, kTagCentroid = 3, kTagEnv = 4 };
+
+struct Key {
+  uint32_t k0, k1;
+};
+
+__device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                        Key key) {
+  uint32_t k0 = key.k0, k1 = key.k1;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t m0 = (uint64_t)0xD2511F53u * c0;   // one v_mad_u64_u32 each
+    const uint64_t m1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+    c0 = n0;
+    c1 = (uint32_t)m1;
+    c2 = n2;
+    c3 = (uint32_t)m0;
+    k0 += 0x9E3779B9u;                                 // Weyl schedule; the key is
+    k1 += 0xBB67AE85u;                                 // wave-uniform (scalar unit)
+  }
+  return make_uint4(c0, c1, c2, c3);
+}
+
+__device__ __forceinline__ float unit24(uint32_t x) {        // [0, 1)
+  return (float)(x >> 8) * 0x1p-24f;
+}
+__device__ __forceinline__ float unit24_open0(uint32_t x) {  // (0, 1]
+  return (float)((x >> 8) + 1u) * 0x1p-24f;
+}
+
+// ---------------------------------------------------------------------------
+// fp32 functions from +, -, *, fma, IEEE division and square root.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float fma32(float a, float b, float c) {
+  return __builtin_fmaf(a, b, c);
+}
+
+constexpr float kLn2Hi = 0x1.62e4p-1f;      // ln 2, 16 leading bits
+constexpr float kLn2Lo = 0x1.7f7d1cp-20f;   // remainder of ln 2
+constexpr float kPi = 0x1.921fb6p+1f;
+constexpr float kHalfPi = 0x1.921fb6p+0f;
+constexpr float kLog2e = 0x1.715476p+0f;
+
+// ln x for positive normal x.  x = 2^e m, m folded into [sqrt(1/2), sqrt(2));
+// ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd series through s^9.
+__device__ __forceinline__ float log_pos(float x) {
+  const uint32_t bits = __float_as_uint(x);
+  const uint32_t frac = bits & 0x7fffffu;
+  const bool fold = frac > 0x3504f3u;
+  const int e = (int)(bits >> 23) - 127 + (fold ? 1 : 0);
+  const float m = __uint_as_float((frac | 0x3f800000u) - (fold ? 0x00800000u : 0u));
+  const float s = (m - 1.0f) / (m + 1.0f);
+  const float s2 = s * s;
+  float p = fma32(s2, 2.0f / 9.0f, 2.0f / 7.0f);
+  p = fma32(s2, p, 2.0f / 5.0f);
+  p = fma32(s2, p, 2.0f / 3.0f);
+  const float lnm = fma32(s * s2, p, s + s);
+  const float fe = (float)e;
+  return fma32(fe, kLn2Hi, fma32(fe, kLn2Lo, lnm));
+}
+
+// sin / cos of x, |x| <= pi/4: Taylor polynomials through x^9 and x^10.
+__device__ __forceinline__ float sin_small(float x) {
+  const float x2 = x * x;
+  float p = fma32(x2, 1.0f / 362880.0f, -1.0f / 5040.0f);
+  p = fma32(x2, p, 1.0f / 120.0f);
+  p = fma32(x2, p, -1.0f / 6.0f);
+  return fma32(x * x2, p, x);
+}
+__device__ __forceinline__ float cos_small(float x) {
+  const float x2 = x * x;
+  float p = fma32(x2, -1.0f / 3628800.0f, 1.0f / 40320.0f);
+  p = fma32(x2, p, -1.0f / 720.0f);
+  p = fma32(x2, p, 1.0f / 24.0f);
+  p = fma32(x2, p, -0.5f);
+  return fma32(x2, p, 1.0f);
+}
+
+// (cos, sin) of 2 pi m / 2^24 for a 24-bit m: the nearest quarter turn q
+// (halves rounding up) is split off in integers, leaving (pi/2) f with
+// f = m / 2^22 - q, |f| <= 1/2, exactly.
+__device__ __forceinline__ float2 turn_cos_sin(uint32_t m) {
+  const uint32_t q = (m + 0x200000u) >> 22;
+  const float f = (float)((int32_t)m - (int32_t)(q << 22)) * 0x1p-22f;
+  const float x = f * kHalfPi;
+  const float s = sin_small(x), c = cos_small(x);
+  switch (q & 3u) {
+    case 0: return make_float2(c, s);
+    case 1: return make_float2(-s, c);
+    case 2: return make_float2(-c, -s);
+    default: return make_float2(s, -c);
+  }
+}
+
+// Two standard normals (Box-Muller) from two Philox words.
+__device__ __forceinline__ float2 gauss2(uint32_t xa, uint32_t xb) {
+  const float r = __builtin_sqrtf(-2.0f * log_pos(unit24_open0(xa)));
+  const float2 cs = turn_cos_sin(xb >> 8);
+  return make_float2(r * cs.x, r * cs.y);
+}
+
+// sin(pi x) up to sign: r = x - rint(x) (exact), y = pi r, Taylor to y^13.
+__device__ __forceinline__ float sinpi_unsigned(float x) {
+  const float r = x - __builtin_rintf(x);
+  const float y = r * kPi;
+  const float y2 = y * y;
+  float p = fma32(y2, 1.0f / 6227020800.0f, -1.0f / 39916800.0f);
+  p = fma32(y2, p, 1.0f / 362880.0f);
+  p = fma32(y2, p, -1.0f / 5040.0f);
+  p = fma32(y2, p, 1.0f / 120.0f);
+  p = fma32(y2, p, -1.0f / 6.0f);
+  return fma32(y * y2, p, y);
+}
+
+// e^x, input clamped to [-87, 88]: k = rint(x log2 e), r = x - k ln 2 in two
+// fma steps, Taylor through r^7, times 2^k assembled in the exponent field.
+__device__ __forceinline__ float exp32(float x) {
+  const float y = x < -87.0f ? -87.0f : (x > 88.0f ? 88.0f : x);
+  const float k = __builtin_rintf(y * kLog2e);
+  float r = fma32(-k, kLn2Hi, y);
+  r = fma32(-k, kLn2Lo, r);
+  float p = fma32(r, 1.0f / 5040.0f, 1.0f / 720.0f);
+  p = fma32(r, p, 1.0f / 120.0f);
+  p = fma32(r, p, 1.0f / 24.0f);
+  p = fma32(r, p, 1.0f / 6.0f);
+  p = fma32(r, p, 0.5f);
+  p = fma32(r, p, 1.0f);
+  p = fma32(r, p, 1.0f);
+  const float scale = __uint_as_float((uint32_t)((int32_t)k + 127) << 23);
+  const float e = p * scale;
+  return x == x ? e : x;
+}
+
+// tanh: odd Taylor polynomial through x^11 for |x| < 0.3,
+// else 1 - 2 / (e^{2|x|} + 1); the sign is copied back.
+__device__ __forceinline__ float tanh32(float x) {
+  const float a = __builtin_fabsf(x);
+  float r;
+  if (a < 0.3f) {
+    const float a2 = a * a;
+    float p = fma32(a2, -1382.0f / 155925.0f, 62.0f / 2835.0f);
+    p = fma32(a2, p, -17.0f / 315.0f);
+    p = fma32(a2, p, 2.0f / 15.0f);
+    p = fma32(a2, p, -1.0f / 3.0f);
+    r = fma32(a * a2, p, a);
+  } else {
+    r = 1.0f - 2.0f / (exp32(a + a) + 1.0f);
+  }
+  return __builtin_copysignf(r, x);
+}
+
+__device__ __forceinline__ float sigmoid32(float x) { return 1.0f / (1.0f + exp32(-x)); }
+
+// ---------------------------------------------------------------------------
+// Wave64 helpers.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Pairwise fold of one value per lane: after the steps h = 32, 16, ..., 1
+// (lane l adds lane l + h), lane 0 holds the total in that fixed order.
+__device__ __forceinline__ float wave_fold_sum(float v) {
+#pragma unroll
+  for (int h = 32; h >= 1; h >>= 1) v = v + __shfl_down(v, h, 64);
+  return v;
+}
+
+// Order-preserving map of an fp32 objective to u32 (-0 folded onto +0).
+__device__ __forceinline__ uint32_t order_bits(float f) {
+  const uint32_t u = __float_as_uint(f == 0.0f ? 0.0f : f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace qd

@@ -1,0 +1,526 @@
+// qd_kernels.hpp -- HIP kernels of one MAP-Elites generation for gfx950.
+//
+// Pipeline of one generation (Algorithm 1 after the first iteration; the
+// first iteration runs the same kernels with the random-init genotype):
+//   k_vary_eval     one wave64 per offspring: draw two parents uniformly from
+//                   the filled cells (Appendix A.2), Iso+LineDD (Algorithm 2)
+//                   gene by gene on coalesced float4 rows of both parents, and
+//                   the objective/descriptor reduction (Appendix B.2) in the
+//                   same pass.  Offspring genotypes are not stored.
+//   k_cell_insert   one thread per offspring: descriptor -> cell (grid bin or
+//                   exact nearest CVT centroid through a bucket grid), then a
+//                   wave-aggregated 64-bit atomicMax of the packed key
+//                   (objective order bits, N_B-1-j) into the cell.
+//   k_regen         one wave per cell: a cell whose key now names an
+//                   offspring regenerates that offspring's genotype into the
+//                   cell's *other* genotype bank (parents stay readable in the
+//                   current bank, so no copy of the batch is ever made).
+//   k_finalize      one workgroup: flip the bank of every new elite, turn its
+//                   key into the incumbent form, and compact the filled cells
+//                   into the ascending list the next selection draws from.
+#pragma once
+
+#include "qd_device.hpp"
+
+namespace qd {
+
+constexpr int kTaskRastrigin = 0, kTaskSphere = 1, kTaskProj = 2, kTaskMlp = 3;
+constexpr int kTessGrid = 0, kTessCvt = 1;
+
+struct Params {
+  int task, tess, n, nb, D, C, stride;
+  int grid[4];
+  float lo[4], hi[4], span[4];    // span = hi - lo in fp32
+  float iso_sigma, line_sigma, init_lo, init_span;
+  int obs, hid, act, T;
+  Key key;
+  int bucket_res, num_buckets;
+  uint64_t* arch_key;
+  float* arch_fit;
+  float* arch_desc;
+  uint32_t* arch_slot;
+  float* arch_geno;               // [2][C][stride]
+  float* cent;                    // [C][D]
+  int* bucket_start;              // [num_buckets + 1], then [num_buckets] cursors
+  float4* bucket_pts;             // [C]
+  int* bucket_idx;                // [C]
+  float* env;
+  int* occ_list;
+  int* counters;                  // [0] filled cells, [1] flags
+  int* off_par;
+  float* off_fit;
+  float* off_desc;
+  int* off_cell;
+  uint8_t* off_won;
+  float* off_geno;                // [N_B][stride] or null
+  double* stats;
+};
+
+__device__ __forceinline__ float* geno_row(const Params& p, uint32_t bank, int cell) {
+  return p.arch_geno + ((size_t)bank * (size_t)p.C + (size_t)cell) * (size_t)p.stride;
+}
+
+__device__ __forceinline__ int pick(const int* occ_list, uint32_t x, int nocc) {
+  return occ_list[(uint32_t)(((uint64_t)x * (uint32_t)nocc) >> 32)];
+}
+
+// Parents and line coefficient of offspring j in generation g >= 1.
+struct Pair {
+  const float* row1;
+  const float* row2;
+  float lambda;
+  int c1, c2;
+};
+
+__device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, int nocc) {
+  const uint4 x = philox(0u, (uint32_t)j, g, kTagSelect, p.key);
+  Pair q;
+  q.c1 = pick(p.occ_list, x.x, nocc);
+  q.c2 = pick(p.occ_list, x.y, nocc);
+  q.lambda = p.line_sigma * gauss2(x.z, x.w).x;
+  q.row1 = geno_row(p, p.arch_slot[q.c1], q.c1);
+  q.row2 = geno_row(p, p.arch_slot[q.c2], q.c2);
+  return q;
+}
+
+// Genes base..base+3 of offspring j (base a multiple of 4).  GEN0: the random
+// first batch of a test function, lo + U (hi - lo).  Otherwise Algorithm 2:
+// theta1 + sigma1 eps1 + lambda (theta2 - theta1), eps1 from block base/4.
+template <bool GEN0>
+__device__ __forceinline__ float4 make_genes(const Params& p, const Pair& q, uint32_t g, int j,
+                                             int base) {
+  if (GEN0) {
+    const uint4 x = philox((uint32_t)(base >> 2), (uint32_t)j, 0u, kTagInit, p.key);
+    return make_float4(fma32(unit24(x.x), p.init_span, p.init_lo),
+                       fma32(unit24(x.y), p.init_span, p.init_lo),
+                       fma32(unit24(x.z), p.init_span, p.init_lo),
+                       fma32(unit24(x.w), p.init_span, p.init_lo));
+  } else {
+    const float4 t1 = *reinterpret_cast<const float4*>(q.row1 + base);
+    const float4 t2 = *reinterpret_cast<const float4*>(q.row2 + base);
+    const uint4 x = philox((uint32_t)(base >> 2), (uint32_t)j, g, kTagIso, p.key);
+    const float2 e01 = gauss2(x.x, x.y);
+    const float2 e23 = gauss2(x.z, x.w);
+    const float s1 = p.iso_sigma, l = q.lambda;
+    return make_float4(fma32(l, t2.x - t1.x, fma32(s1, e01.x, t1.x)),
+                       fma32(l, t2.y - t1.y, fma32(s1, e01.y, t1.y)),
+                       fma32(l, t2.z - t1.z, fma32(s1, e23.x, t1.z)),
+                       fma32(l, t2.w - t1.w, fma32(s1, e23.y, t1.w)));
+  }
+}
+
+__device__ __forceinline__ float clip(float x, float lo, float hi) {
+  return __builtin_fminf(__builtin_fmaxf(x, lo), hi);
+}
+
+template <int TASK>
+__device__ __forceinline__ float task_term(float x) {
+  if (TASK == kTaskSphere) return x * x;
+  const float s = sinpi_unsigned(x);
+  return fma32(20.0f, s * s, x * x);
+}
+
+// ---------------------------------------------------------------------------
+// Select + vary + evaluate, one wave per offspring (test functions).
+// Lane l owns genes 256c + 4l .. 256c + 4l + 3 of every chunk c, i.e. gene
+// groups q = g/4 with q mod 64 = l; its partial sums run in ascending gene
+// order and the wave folds them pairwise (h = 32 .. 1).
+// ---------------------------------------------------------------------------
+template <int TASK, bool GEN0, bool KEEP>
+__global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
+  const int lane = threadIdx.x & 63;
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= p.nb) return;
+
+  Pair q{nullptr, nullptr, 0.0f, -1, -1};
+  if (!GEN0) {
+    const int nocc = p.counters[0];
+    if (nocc <= 0) {
+      if (lane == 0) {
+        p.off_fit[j] = __builtin_nanf("");
+        p.off_par[2 * j] = -1;
+        p.off_par[2 * j + 1] = -1;
+        p.off_won[j] = 0;
+        atomicOr(reinterpret_cast<unsigned int*>(p.counters + 1), 1u);
+      }
+      return;
+    }
+    q = select_pair(p, g, j, nocc);
+  }
+
+  const int n = p.n;
+  const int half = n >> 1;
+  float acc = 0.0f, dlo = 0.0f, dhi = 0.0f;
+  float g0 = 0.0f, g1 = 0.0f;
+  float* keep_row = KEEP ? p.off_geno + (size_t)j * (size_t)p.stride : nullptr;
+  for (int base = 4 * lane; base < n; base += 256) {
+    const float4 v4 = make_genes<GEN0>(p, q, g, j, base);
+    if (KEEP) *reinterpret_cast<float4*>(keep_row + base) = v4;
+    const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+    if (base == 0) {
+      g0 = v[0];
+      g1 = v[1];
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int gi = base + k;
+      if (gi < n) {
+        acc = acc + task_term<TASK>(v[k]);
+        if (TASK == kTaskProj) {
+          if (gi < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
+          else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+        }
+      }
+    }
+  }
+  const float total = wave_fold_sum(acc);
+  float d0, d1;
+  if (TASK == kTaskProj) {
+    d0 = wave_fold_sum(dlo) / (float)half;
+    d1 = wave_fold_sum(dhi) / (float)(n - half);
+  } else {
+    d0 = clip(g0, p.lo[0], p.hi[0]);
+    d1 = clip(g1, p.lo[1], p.hi[1]);
+  }
+  if (lane == 0) {
+    p.off_fit[j] = -total;
+    p.off_desc[2 * j] = d0;
+    p.off_desc[2 * j + 1] = d1;
+    p.off_par[2 * j] = q.c1;
+    p.off_par[2 * j + 1] = q.c2;
+    p.off_won[j] = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Descriptor -> cell.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int grid_cell(const Params& p, const float* d) {
+  int cell = 0;
+  for (int k = 0; k < p.D; ++k) {
+    if (!(d[k] == d[k])) return -1;
+    const float t = (d[k] - p.lo[k]) / p.span[k];
+    const float fb = __builtin_floorf(t * (float)p.grid[k]);
+    const int b = fb < 0.0f ? 0 : (fb > (float)(p.grid[k] - 1) ? p.grid[k] - 1 : (int)fb);
+    cell = cell * p.grid[k] + b;
+  }
+  return cell;
+}
+
+// Exact nearest centroid (squared distance as an fma chain over dimensions,
+// ties to the lowest index) through a bucket grid of bucket_res^D cells over
+// the unit box.  Rings of buckets around the query's bucket are visited in
+// Chebyshev order until the best distance found is certainly below the
+// distance to every unvisited bucket (with a relative margin far above the
+// fp32 rounding of either side), so the answer equals the brute-force argmin.
+__device__ int cvt_cell(const Params& p, const float* d) {
+  const int D = p.D, R = p.bucket_res;
+  float u[4];
+  int qb[4];
+  for (int k = 0; k < D; ++k) {
+    if (!(d[k] == d[k])) return -1;
+    u[k] = (d[k] - p.lo[k]) / p.span[k];
+    float fb = __builtin_floorf(u[k] * (float)R);
+    fb = fb < 0.0f ? 0.0f : (fb > (float)(R - 1) ? (float)(R - 1) : fb);
+    qb[k] = (int)fb;
+  }
+  float best = __builtin_inff();
+  int best_idx = 0x7fffffff;
+  const double invR = 1.0 / (double)R;
+  for (int r = 0; r < R; ++r) {
+    const int side = 2 * r + 1;
+    int span_n = 1;
+    for (int k = 0; k < D; ++k) span_n *= side;
+    for (int e = 0; e < span_n; ++e) {
+      int rest = e, bucket = 0, cheb = 0;
+      bool inside = true;
+      for (int k = 0; k < D; ++k) {
+        const int off = rest % side - r;
+        rest /= side;
+        const int b = qb[k] + off;
+        if (b < 0 || b >= R) inside = false;
+        const int a = off < 0 ? -off : off;
+        cheb = a > cheb ? a : cheb;
+        bucket = bucket * R + b;
+      }
+      if (!inside || cheb != r) continue;
+      const int s0 = p.bucket_start[bucket], s1 = p.bucket_start[bucket + 1];
+      for (int s = s0; s < s1; ++s) {
+        const float4 c = p.bucket_pts[s];
+        const float cc[4] = {c.x, c.y, c.z, c.w};
+        float acc = 0.0f;
+        for (int k = 0; k < D; ++k) {
+          const float diff = u[k] - cc[k];
+          acc = fma32(diff, diff, acc);
+        }
+        const int idx = p.bucket_idx[s];
+        if (acc < best || (acc == best && idx < best_idx)) {
+          best = acc;
+          best_idx = idx;
+        }
+      }
+    }
+    // lower bound on the distance to anything outside the visited box
+    double bound = __builtin_inf();
+    bool face = false;
+    for (int k = 0; k < D; ++k) {
+      if (qb[k] - r >= 1) {
+        const double gap = (double)u[k] - (double)(qb[k] - r) * invR - 1e-6;
+        bound = fmin(bound, gap > 0.0 ? gap * gap : 0.0);
+        face = true;
+      }
+      if (qb[k] + r + 1 <= R - 1) {
+        const double gap = (double)(qb[k] + r + 1) * invR - (double)u[k] - 1e-6;
+        bound = fmin(bound, gap > 0.0 ? gap * gap : 0.0);
+        face = true;
+      }
+    }
+    if (!face) break;
+    if (best_idx != 0x7fffffff && (double)best * (1.0 + 1e-5) < bound) break;
+  }
+  return best_idx;
+}
+
+template <int TESS>
+__global__ __launch_bounds__(256) void k_cell_insert(const Params p) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  int cell = -1;
+  uint64_t key = 0;
+  if (j < p.nb) {
+    const float f = p.off_fit[j];
+    if (f == f) {
+      float d[4];
+      for (int k = 0; k < p.D; ++k) d[k] = p.off_desc[(size_t)j * p.D + k];
+      cell = TESS == kTessGrid ? grid_cell(p, d) : cvt_cell(p, d);
+    }
+    p.off_cell[j] = cell;
+    if (cell >= 0)
+      key = ((uint64_t)order_bits(f) << 32) | (uint64_t)(uint32_t)(p.nb - 1 - j);
+  }
+  // one atomic per distinct cell per wave: the lanes that share the leader's
+  // cell fold their keys with max, the leader issues the atomic.
+  uint64_t todo = __ballot(cell >= 0);
+  while (todo) {
+    const int leader = __ffsll((unsigned long long)todo) - 1;
+    const int c = __shfl(cell, leader, 64);
+    const uint64_t same = __ballot(cell == c);
+    uint64_t k = cell == c ? key : 0ull;
+#pragma unroll
+    for (int h = 32; h >= 1; h >>= 1) {
+      const uint64_t o = __shfl_xor(k, h, 64);
+      k = o > k ? o : k;
+    }
+    if (lane_id() == leader) atomicMax((unsigned long long*)&p.arch_key[c], (unsigned long long)k);
+    todo &= ~same;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Winners: one wave per cell regenerates the winning offspring's genotype into
+// the cell's other bank and records its objective and descriptor.
+// ---------------------------------------------------------------------------
+template <bool GEN0>
+__global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (c >= p.C) return;
+  const uint64_t key = p.arch_key[c];
+  const uint32_t low = (uint32_t)key;
+  if (key == 0ull || low == 0xffffffffu) return;
+  const int j = p.nb - 1 - (int)low;
+  Pair q{nullptr, nullptr, 0.0f, -1, -1};
+  if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
+  float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
+  for (int base = 4 * lane; base < p.n; base += 256)
+    *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
+  if (lane == 0) {
+    p.arch_fit[c] = p.off_fit[j];
+    for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
+    p.off_won[j] = 1;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Finalize: new elites switch bank and become incumbents (low word all ones,
+// so a later offspring needs a strictly greater objective); then the filled
+// cells are compacted in ascending order.  One workgroup of 1024 threads.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_finalize(const Params p) {
+  __shared__ int wave_cnt[16];
+  __shared__ int base_sh;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) base_sh = 0;
+  __syncthreads();
+  for (int start = 0; start < p.C; start += 1024) {
+    const int c = start + tid;
+    bool filled = false;
+    if (c < p.C) {
+      const uint64_t key = p.arch_key[c];
+      if (key != 0ull) {
+        filled = true;
+        if ((uint32_t)key != 0xffffffffu) {
+          p.arch_slot[c] ^= 1u;
+          p.arch_key[c] = key | 0xffffffffull;
+        }
+      }
+    }
+    const uint64_t bal = __ballot(filled);
+    const int below = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wave_cnt[wave] = __popcll(bal);
+    __syncthreads();
+    int off = base_sh;
+    for (int w = 0; w < wave; ++w) off += wave_cnt[w];
+    if (filled) p.occ_list[off + below] = c;
+    __syncthreads();
+    if (tid == 0) {
+      int tot = 0;
+      for (int w = 0; w < 16; ++w) tot += wave_cnt[w];
+      base_sh += tot;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) p.counters[0] = base_sh;
+}
+
+// ---------------------------------------------------------------------------
+// Statistics over the archive (fp64 accumulation).  One workgroup.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_stats(const Params p, double offset) {
+  __shared__ double s_sum[16];
+  __shared__ double s_best[16];
+  __shared__ int s_cnt[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  double sum = 0.0, best = -__builtin_inf();
+  int cnt = 0;
+  for (int c = tid; c < p.C; c += 1024) {
+    if (p.arch_key[c] != 0ull) {
+      const double f = (double)p.arch_fit[c];
+      sum += f + offset;
+      best = f > best ? f : best;
+      ++cnt;
+    }
+  }
+  for (int h = 32; h >= 1; h >>= 1) {
+    sum += __shfl_xor(sum, h, 64);
+    const double ob = __shfl_xor(best, h, 64);
+    best = ob > best ? ob : best;
+    cnt += __shfl_xor(cnt, h, 64);
+  }
+  if (lane == 0) {
+    s_sum[wave] = sum;
+    s_best[wave] = best;
+    s_cnt[wave] = cnt;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double ts = 0.0, tb = -__builtin_inf();
+    int tc = 0;
+    for (int w = 0; w < 16; ++w) {
+      ts += s_sum[w];
+      tb = s_best[w] > tb ? s_best[w] : tb;
+      tc += s_cnt[w];
+    }
+    p.stats[0] = ts;
+    p.stats[1] = (double)tc;
+    p.stats[2] = tc ? tb : __builtin_nan("");
+    p.stats[3] = (double)p.counters[1];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Set-up kernels (first iteration only).
+// ---------------------------------------------------------------------------
+__global__ void k_clear_archive(const Params p, int clear_geno) {
+  const size_t tid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t nthr = (size_t)gridDim.x * blockDim.x;
+  for (size_t c = tid; c < (size_t)p.C; c += nthr) {
+    p.arch_key[c] = 0ull;
+    p.arch_fit[c] = __builtin_nanf("");
+    p.arch_slot[c] = 0u;
+    p.occ_list[c] = 0;
+    for (int k = 0; k < p.D; ++k) p.arch_desc[c * p.D + k] = 0.0f;
+  }
+  if (clear_geno) {
+    const size_t nv = (size_t)2 * p.C * p.stride / 4;
+    float4* gp = reinterpret_cast<float4*>(p.arch_geno);
+    for (size_t i = tid; i < nv; i += nthr) gp[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (tid < 64) p.counters[tid] = 0;
+  if (p.num_buckets > 0)
+    for (size_t b = tid; b < (size_t)2 * (p.num_buckets + 1); b += nthr) p.bucket_start[b] = 0;
+}
+
+__device__ __forceinline__ int centroid_bucket(const Params& p, const float* c) {
+  int b = 0;
+  for (int k = 0; k < p.D; ++k) {
+    int bk = (int)(c[k] * (float)p.bucket_res);
+    bk = bk > p.bucket_res - 1 ? p.bucket_res - 1 : bk;
+    b = b * p.bucket_res + bk;
+  }
+  return b;
+}
+
+// Centroid i, coordinate k = 24-bit uniform of word k of block (i, 0, 0, CENTROID).
+__global__ void k_centroids(const Params p) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= p.C) return;
+  const uint4 x = philox((uint32_t)i, 0u, 0u, kTagCentroid, p.key);
+  const float c[4] = {unit24(x.x), unit24(x.y), unit24(x.z), unit24(x.w)};
+  for (int k = 0; k < p.D; ++k) p.cent[(size_t)i * p.D + k] = c[k];
+  atomicAdd(&p.bucket_start[centroid_bucket(p, c) + 1], 1);
+}
+
+__global__ __launch_bounds__(1024) void k_bucket_scan(const Params p) {
+  // inclusive scan of counts stored at [1..NB] -> starts; single workgroup
+  __shared__ int carry;
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) carry = 0;
+  __syncthreads();
+  const int NB = p.num_buckets;
+  for (int start = 1; start <= NB; start += 1024) {
+    const int i = start + tid;
+    int v = i <= NB ? p.bucket_start[i] : 0;
+    for (int h = 1; h < 64; h <<= 1) {
+      const int o = __shfl_up(v, h, 64);
+      if (lane >= h) v += o;
+    }
+    if (lane == 63) wsum[wave] = v;
+    __syncthreads();
+    int off = carry;
+    for (int w = 0; w < wave; ++w) off += wsum[w];
+    if (i <= NB) p.bucket_start[i] = v + off;
+    __syncthreads();
+    if (tid == 0) {
+      int t = 0;
+      for (int w = 0; w < 16; ++w) t += wsum[w];
+      carry += t;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void k_bucket_fill(const Params p) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= p.C) return;
+  float c[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < p.D; ++k) c[k] = p.cent[(size_t)i * p.D + k];
+  const int b = centroid_bucket(p, c);
+  int* cursor = p.bucket_start + (p.num_buckets + 1);
+  const int slot = p.bucket_start[b] + atomicAdd(&cursor[b], 1);
+  p.bucket_pts[slot] = make_float4(c[0], c[1], c[2], c[3]);
+  p.bucket_idx[slot] = i;
+}
+
+// Entry e of [A | B | s0] = 0.1 * normal (e mod 4) of block (e/4, 0, 0, ENV).
+__global__ void k_env(const Params p, int count) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (4 * b >= count) return;
+  const uint4 x = philox((uint32_t)b, 0u, 0u, kTagEnv, p.key);
+  const float2 z01 = gauss2(x.x, x.y), z23 = gauss2(x.z, x.w);
+  const float z[4] = {z01.x, z01.y, z23.x, z23.y};
+  for (int k = 0; k < 4; ++k)
+    if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
+}
+
+}  // namespace qd

@@ -1,0 +1,438 @@
+// qd_lib.hip -- host side of libqd.so: config validation, workspace layout,
+// launch sequencing on the caller's stream, per-kernel event timing and error
+// mapping.  The C ABI is declared in include/qd.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/qd.h"
+#include "qd_kernels.hpp"
+#include "qd_rollout.hpp"
+
+namespace {
+
+thread_local hipError_t g_last_hip = hipSuccess;
+
+constexpr uint64_t kAlign = 256;
+
+uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+bool is_mlp(const qd_config* c) { return c->task == QD_TASK_MLP_SYNTH; }
+
+int32_t genotype_len(const qd_config* c) {
+  if (!is_mlp(c)) return c->genotype_dim;
+  const int64_t o = c->mlp_obs, h = c->mlp_hidden, a = c->mlp_act;
+  const int64_t n = h * o + h + h * h + h + a * h + a;
+  return n > (int64_t)0x7fffffff ? -1 : (int32_t)n;
+}
+
+// Largest R with R^D <= C: about one centroid per bucket.
+int bucket_res_for(int C, int D) {
+  int R = 1;
+  for (;;) {
+    int64_t p = 1;
+    for (int k = 0; k < D; ++k) p *= (R + 1);
+    if (p > C) break;
+    ++R;
+  }
+  return R;
+}
+
+bool finite(float x) { return std::isfinite(x); }
+
+qd_status validate(const qd_config* c) {
+  if (!c) return QD_ERR_INVALID_ARG;
+  if (c->abi_version != QD_ABI_VERSION) return QD_ERR_INVALID_ARG;
+  if (c->task < QD_TASK_RASTRIGIN || c->task > QD_TASK_MLP_SYNTH) return QD_ERR_INVALID_ARG;
+  if (c->tess != QD_TESS_GRID && c->tess != QD_TESS_CVT) return QD_ERR_INVALID_ARG;
+  if (c->batch_size < 1) return QD_ERR_INVALID_ARG;
+  if (c->num_cells < 1 || c->num_cells > (1 << 28)) return QD_ERR_INVALID_ARG;
+  if (c->keep_offspring != 0 && c->keep_offspring != 1) return QD_ERR_INVALID_ARG;
+  const int D = c->desc_dim;
+  if (is_mlp(c)) {
+    if (c->genotype_dim != 0 || D != 4) return QD_ERR_INVALID_ARG;
+    if (c->mlp_obs < 5 || c->mlp_hidden < 1 || c->mlp_act < 1 || c->episode_len < 1)
+      return QD_ERR_INVALID_ARG;
+  } else {
+    if (c->genotype_dim < 2 || D != 2) return QD_ERR_INVALID_ARG;
+    if (!finite(c->init_lo) || !finite(c->init_hi) || !(c->init_lo < c->init_hi))
+      return QD_ERR_INVALID_ARG;
+  }
+  for (int k = 0; k < D; ++k)
+    if (!finite(c->desc_lo[k]) || !finite(c->desc_hi[k]) || !(c->desc_lo[k] < c->desc_hi[k]))
+      return QD_ERR_INVALID_ARG;
+  if (!finite(c->iso_sigma) || !finite(c->line_sigma)) return QD_ERR_INVALID_ARG;
+  if (c->tess == QD_TESS_GRID) {
+    int64_t prod = 1;
+    for (int k = 0; k < D; ++k) {
+      if (c->grid_shape[k] < 1) return QD_ERR_INVALID_ARG;
+      prod *= c->grid_shape[k];
+      if (prod > (int64_t)1 << 31) return QD_ERR_INVALID_ARG;
+    }
+    if (prod != c->num_cells) return QD_ERR_INVALID_ARG;
+  }
+  if (genotype_len(c) < 1) return QD_ERR_INVALID_ARG;
+  if (is_mlp(c) && !qd::rollout_supported(c->mlp_obs, c->mlp_hidden, c->mlp_act))
+    return QD_ERR_UNSUPPORTED;
+  return QD_OK;
+}
+
+qd_status make_layout(const qd_config* c, qd_layout* L) {
+  std::memset(L, 0, sizeof(*L));
+  const uint64_t C = (uint64_t)c->num_cells, D = (uint64_t)c->desc_dim,
+                 nb = (uint64_t)c->batch_size;
+  const int32_t n = genotype_len(c);
+  const uint64_t stride = align_up((uint64_t)n, 64);
+  if (stride > 0x7fffffffull) return QD_ERR_INVALID_ARG;
+  L->genotype_dim = n;
+  L->row_stride = (int32_t)stride;
+  if (c->tess == QD_TESS_CVT) {
+    L->bucket_res = bucket_res_for(c->num_cells, c->desc_dim);
+    int64_t nbk = 1;
+    for (uint64_t k = 0; k < D; ++k) nbk *= L->bucket_res;
+    L->num_buckets = (int32_t)nbk;
+  }
+  const uint64_t env = is_mlp(c) ? (uint64_t)c->mlp_obs * (c->mlp_obs + c->mlp_act + 1) : 0;
+  uint64_t bytes[QD_NUM_BUFFERS] = {};
+  // overflow guard: every product below stays far under 2^63 for these limits
+  if (nb > ((uint64_t)1 << 31) || stride * (nb + 2 * C) > ((uint64_t)1 << 60))
+    return QD_ERR_INVALID_ARG;
+  bytes[QD_BUF_ARCHIVE_KEY] = 8 * C;
+  bytes[QD_BUF_ARCHIVE_FIT] = 4 * C;
+  bytes[QD_BUF_ARCHIVE_DESC] = 4 * C * D;
+  bytes[QD_BUF_ARCHIVE_SLOT] = 4 * C;
+  bytes[QD_BUF_ARCHIVE_GENO] = 4 * 2 * C * stride;
+  bytes[QD_BUF_CENTROIDS] = c->tess == QD_TESS_CVT ? 4 * C * D : 0;
+  bytes[QD_BUF_BUCKET_START] = c->tess == QD_TESS_CVT ? 4 * 2 * ((uint64_t)L->num_buckets + 1) : 0;
+  bytes[QD_BUF_BUCKET_ITEMS] = c->tess == QD_TESS_CVT ? (16 + 4) * C : 0;
+  bytes[QD_BUF_ENV] = 4 * env;
+  bytes[QD_BUF_OCC_LIST] = 4 * C;
+  bytes[QD_BUF_COUNTERS] = 4 * 64;
+  bytes[QD_BUF_OFF_PARENTS] = 4 * 2 * nb;
+  bytes[QD_BUF_OFF_FIT] = 4 * nb;
+  bytes[QD_BUF_OFF_DESC] = 4 * nb * D;
+  bytes[QD_BUF_OFF_CELL] = 4 * nb;
+  bytes[QD_BUF_OFF_WON] = nb;
+  bytes[QD_BUF_OFF_GENO] = c->keep_offspring ? 4 * nb * stride : 0;
+  bytes[QD_BUF_STATS] = 8 * 8;
+  uint64_t off = 0;
+  for (int b = 0; b < QD_NUM_BUFFERS; ++b) {
+    L->offset[b] = off;
+    L->bytes[b] = bytes[b];
+    off = align_up(off + bytes[b], kAlign);
+  }
+  L->workspace_bytes = off;
+  return QD_OK;
+}
+
+}  // namespace
+
+struct qd_archive {
+  qd_config cfg;
+  qd_layout lay;
+  qd::Params p;
+  bool timing = false;
+  struct Rec {
+    int kernel;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+qd_status hip_fail(hipError_t e) {
+  g_last_hip = e;
+  return QD_ERR_HIP;
+}
+
+hipEvent_t take_event(qd_archive* h) {
+  if (!h->pool.empty()) {
+    hipEvent_t e = h->pool.back();
+    h->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Brackets one launch with events when timing is on.
+struct Timed {
+  qd_archive* h;
+  hipStream_t s;
+  int kernel;
+  hipEvent_t a = nullptr;
+  Timed(qd_archive* h_, hipStream_t s_, int k) : h(h_), s(s_), kernel(k) {
+    if (h->timing) {
+      a = take_event(h);
+      if (a) (void)hipEventRecord(a, s);
+    }
+  }
+  ~Timed() {
+    if (h->timing && a) {
+      hipEvent_t b = take_event(h);
+      if (b) {
+        (void)hipEventRecord(b, s);
+        h->recs.push_back({kernel, a, b});
+      } else {
+        h->pool.push_back(a);
+      }
+    }
+  }
+};
+
+unsigned blocks_for(uint64_t items, unsigned per_block) {
+  return (unsigned)((items + per_block - 1) / per_block);
+}
+
+template <bool GEN0>
+void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
+  const qd::Params& p = h->p;
+  const dim3 grid(blocks_for((uint64_t)p.nb, 4)), block(256);
+  Timed t(h, s, QD_K_VARY_EVAL);
+  const bool keep = h->cfg.keep_offspring != 0;
+#define QD_VE(TASK)                                                                      \
+  do {                                                                                   \
+    if (keep) hipLaunchKernelGGL((qd::k_vary_eval<TASK, GEN0, true>), grid, block, 0, s, p, g); \
+    else hipLaunchKernelGGL((qd::k_vary_eval<TASK, GEN0, false>), grid, block, 0, s, p, g);     \
+  } while (0)
+  switch (p.task) {
+    case qd::kTaskRastrigin: QD_VE(qd::kTaskRastrigin); break;
+    case qd::kTaskSphere: QD_VE(qd::kTaskSphere); break;
+    default: QD_VE(qd::kTaskProj); break;
+  }
+#undef QD_VE
+}
+
+void launch_cell_insert(qd_archive* h, hipStream_t s) {
+  const qd::Params& p = h->p;
+  Timed t(h, s, QD_K_CELL_INSERT);
+  const dim3 grid(blocks_for((uint64_t)p.nb, 256)), block(256);
+  if (p.tess == qd::kTessGrid) hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessGrid>), grid, block, 0, s, p);
+  else hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessCvt>), grid, block, 0, s, p);
+}
+
+template <bool GEN0>
+void launch_regen(qd_archive* h, hipStream_t s, uint32_t g) {
+  const qd::Params& p = h->p;
+  Timed t(h, s, QD_K_REGEN);
+  const dim3 grid(blocks_for((uint64_t)p.C, 4)), block(256);
+  if (p.task == qd::kTaskMlp) qd::launch_mlp_regen(p, GEN0, g, s);
+  else hipLaunchKernelGGL((qd::k_regen<GEN0>), grid, block, 0, s, p, g);
+}
+
+void launch_finalize(qd_archive* h, hipStream_t s) {
+  Timed t(h, s, QD_K_FINALIZE);
+  hipLaunchKernelGGL(qd::k_finalize, dim3(1), dim3(1024), 0, s, h->p);
+}
+
+template <bool GEN0>
+qd_status enqueue_generation(qd_archive* h, hipStream_t s, uint32_t g) {
+  if (h->p.task == qd::kTaskMlp) {
+    Timed t(h, s, QD_K_ROLLOUT);
+    qd::launch_rollout(h->p, GEN0, g, h->cfg.keep_offspring != 0, s);
+  } else {
+    launch_vary_eval<GEN0>(h, s, g);
+  }
+  launch_cell_insert(h, s);
+  launch_regen<GEN0>(h, s, g);
+  launch_finalize(h, s);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? QD_OK : hip_fail(e);
+}
+
+qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
+  qd::Params p;
+  std::memset(&p, 0, sizeof(p));
+  p.task = c->task;
+  p.tess = c->tess;
+  p.n = L->genotype_dim;
+  p.nb = c->batch_size;
+  p.D = c->desc_dim;
+  p.C = c->num_cells;
+  p.stride = L->row_stride;
+  for (int k = 0; k < 4; ++k) {
+    p.grid[k] = c->grid_shape[k];
+    p.lo[k] = c->desc_lo[k];
+    p.hi[k] = c->desc_hi[k];
+    const volatile float hi = c->desc_hi[k], lo = c->desc_lo[k];
+    p.span[k] = hi - lo;  // fp32 subtraction, as the descriptor formula defines it
+  }
+  p.iso_sigma = c->iso_sigma;
+  p.line_sigma = c->line_sigma;
+  p.init_lo = c->init_lo;
+  {
+    const volatile float hi = c->init_hi, lo = c->init_lo;
+    p.init_span = hi - lo;
+  }
+  p.obs = c->mlp_obs;
+  p.hid = c->mlp_hidden;
+  p.act = c->mlp_act;
+  p.T = c->episode_len;
+  p.key.k0 = (uint32_t)(c->seed & 0xffffffffull);
+  p.key.k1 = (uint32_t)(c->seed >> 32);
+  p.bucket_res = L->bucket_res;
+  p.num_buckets = L->num_buckets;
+  auto at = [&](int b) -> void* { return L->bytes[b] ? ws + L->offset[b] : nullptr; };
+  p.arch_key = (uint64_t*)at(QD_BUF_ARCHIVE_KEY);
+  p.arch_fit = (float*)at(QD_BUF_ARCHIVE_FIT);
+  p.arch_desc = (float*)at(QD_BUF_ARCHIVE_DESC);
+  p.arch_slot = (uint32_t*)at(QD_BUF_ARCHIVE_SLOT);
+  p.arch_geno = (float*)at(QD_BUF_ARCHIVE_GENO);
+  p.cent = (float*)at(QD_BUF_CENTROIDS);
+  p.bucket_start = (int*)at(QD_BUF_BUCKET_START);
+  if (L->bytes[QD_BUF_BUCKET_ITEMS]) {
+    p.bucket_pts = (float4*)(ws + L->offset[QD_BUF_BUCKET_ITEMS]);
+    p.bucket_idx = (int*)(ws + L->offset[QD_BUF_BUCKET_ITEMS] + 16ull * c->num_cells);
+  }
+  p.env = (float*)at(QD_BUF_ENV);
+  p.occ_list = (int*)at(QD_BUF_OCC_LIST);
+  p.counters = (int*)at(QD_BUF_COUNTERS);
+  p.off_par = (int*)at(QD_BUF_OFF_PARENTS);
+  p.off_fit = (float*)at(QD_BUF_OFF_FIT);
+  p.off_desc = (float*)at(QD_BUF_OFF_DESC);
+  p.off_cell = (int*)at(QD_BUF_OFF_CELL);
+  p.off_won = (uint8_t*)at(QD_BUF_OFF_WON);
+  p.off_geno = (float*)at(QD_BUF_OFF_GENO);
+  p.stats = (double*)at(QD_BUF_STATS);
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+qd_status qd_layout_query(const qd_config* cfg, qd_layout* out) {
+  if (!out) return QD_ERR_INVALID_ARG;
+  const qd_status st = validate(cfg);
+  if (st != QD_OK) return st;
+  return make_layout(cfg, out);
+}
+
+qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t workspace_bytes,
+                          void* stream, qd_archive** out) {
+  if (!out || !d_workspace) return QD_ERR_INVALID_ARG;
+  *out = nullptr;
+  qd_layout L;
+  qd_status st = qd_layout_query(cfg, &L);
+  if (st != QD_OK) return st;
+  if (((uintptr_t)d_workspace % kAlign) != 0) return QD_ERR_INVALID_ARG;
+  if (workspace_bytes < L.workspace_bytes) return QD_ERR_WORKSPACE_TOO_SMALL;
+  qd_archive* h = new (std::nothrow) qd_archive();
+  if (!h) return QD_ERR_INVALID_ARG;
+  h->cfg = *cfg;
+  h->lay = L;
+  h->p = make_params(cfg, &L, (uint8_t*)d_workspace);
+  hipStream_t s = (hipStream_t)stream;
+  const qd::Params& p = h->p;
+  {
+    Timed t(h, s, QD_K_SETUP);
+    hipLaunchKernelGGL(qd::k_clear_archive, dim3(1024), dim3(256), 0, s, p, 1);
+    if (p.tess == qd::kTessCvt) {
+      hipLaunchKernelGGL(qd::k_centroids, dim3(blocks_for(p.C, 256)), dim3(256), 0, s, p);
+      hipLaunchKernelGGL(qd::k_bucket_scan, dim3(1), dim3(1024), 0, s, p);
+      hipLaunchKernelGGL(qd::k_bucket_fill, dim3(blocks_for(p.C, 256)), dim3(256), 0, s, p);
+    }
+    if (p.task == qd::kTaskMlp) {
+      const int count = p.obs * (p.obs + p.act + 1);
+      hipLaunchKernelGGL(qd::k_env, dim3(blocks_for((count + 3) / 4, 256)), dim3(256), 0, s, p,
+                         count);
+    }
+  }
+  st = enqueue_generation<true>(h, s, 0u);
+  if (st != QD_OK) {
+    delete h;
+    return st;
+  }
+  *out = h;
+  return QD_OK;
+}
+
+qd_status qd_generation(qd_archive* h, uint32_t gen_index, void* stream) {
+  if (!h || gen_index == 0) return QD_ERR_INVALID_ARG;
+  return enqueue_generation<false>(h, (hipStream_t)stream, gen_index);
+}
+
+qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_stats* out) {
+  if (!h || !out) return QD_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  hipLaunchKernelGGL(qd::k_stats, dim3(1), dim3(1024), 0, s, h->p, qd_offset);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e);
+  double host[4];
+  e = hipMemcpyAsync(host, h->p.stats, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e);
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e);
+  out->qd_score = host[0];
+  out->num_occupied = (int32_t)host[1];
+  out->coverage = host[1] / (double)h->cfg.num_cells;
+  out->best_fitness = (float)host[2];
+  out->flags = (uint32_t)host[3];
+  out->reserved = 0;
+  return QD_OK;
+}
+
+qd_status qd_archive_layout(const qd_archive* h, qd_layout* out) {
+  if (!h || !out) return QD_ERR_INVALID_ARG;
+  *out = h->lay;
+  return QD_OK;
+}
+
+qd_status qd_set_kernel_timing(qd_archive* h, int32_t enable) {
+  if (!h) return QD_ERR_INVALID_ARG;
+  h->timing = enable != 0;
+  return QD_OK;
+}
+
+qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts) {
+  if (!h || !ms || !counts) return QD_ERR_INVALID_ARG;
+  for (int k = 0; k < QD_NUM_KERNELS; ++k) {
+    ms[k] = 0.0;
+    counts[k] = 0;
+  }
+  qd_status st = QD_OK;
+  for (auto& r : h->recs) {
+    hipError_t e = hipEventSynchronize(r.b);
+    float t = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess) st = hip_fail(e);
+    ms[r.kernel] += (double)t;
+    counts[r.kernel] += 1;
+    h->pool.push_back(r.a);
+    h->pool.push_back(r.b);
+  }
+  h->recs.clear();
+  return st;
+}
+
+qd_status qd_archive_destroy(qd_archive* h) {
+  if (!h) return QD_OK;
+  for (auto& r : h->recs) {
+    (void)hipEventSynchronize(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : h->pool) (void)hipEventDestroy(e);
+  delete h;
+  return QD_OK;
+}
+
+const char* qd_status_str(qd_status s) {
+  switch (s) {
+    case QD_OK: return "ok";
+    case QD_ERR_INVALID_ARG: return "invalid argument";
+    case QD_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case QD_ERR_EMPTY_ARCHIVE: return "empty archive";
+    case QD_ERR_UNSUPPORTED: return "unsupported configuration";
+    case QD_ERR_HIP: return hipGetErrorString(g_last_hip);
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

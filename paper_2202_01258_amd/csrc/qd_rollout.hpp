@@ -1,0 +1,265 @@
+// qd_rollout.hpp -- policy rollouts on the synthetic dynamics (gfx950).
+//
+// Evaluation of a batch of tanh MLP policies (two hidden tanh layers and a
+// tanh output, as in Section 5.1 of the paper) for T steps of
+// s' = tanh(A s + B a).  Every individual has its own weights, so this is a
+// batch of independent GEMV chains, not one GEMM: no matrix core applies.
+//
+// One workgroup of H threads (H = hidden width, one or two waves) runs one
+// individual.  Thread o keeps row o of W1 and W2 and the biases b1[o], b2[o]
+// in VGPRs for the whole episode; W3 and b3 live in LDS; thread i < obs keeps
+// row i of A and B.  Activations pass through LDS with a barrier per layer.
+// Each output is one fma chain in ascending input order, which keeps the
+// result independent of the launch shape.
+//
+// The genotype is produced in the kernel's prologue straight from the parents
+// (or the Glorot-uniform first batch) -- offspring weights never touch HBM.
+#pragma once
+
+#include "qd_kernels.hpp"
+
+namespace qd {
+
+constexpr int kObs = 27, kAct = 8;
+
+inline bool rollout_supported(int obs, int hid, int act) {
+  return obs == kObs && act == kAct && (hid == 64 || hid == 128);
+}
+
+// Glorot-uniform first-batch gene i (biases are zero).
+__device__ __forceinline__ float mlp_init_gene(const Params& p, int i, float u) {
+  const int o = p.obs, h = p.hid, a = p.act;
+  const int e1 = h * o, e2 = e1 + h, e3 = e2 + h * h, e4 = e3 + h, e5 = e4 + a * h;
+  float lim;
+  if (i < e1) lim = __builtin_sqrtf(6.0f / (float)(o + h));
+  else if (i < e2) lim = 0.0f;
+  else if (i < e3) lim = __builtin_sqrtf(6.0f / (float)(h + h));
+  else if (i < e4) lim = 0.0f;
+  else if (i < e5) lim = __builtin_sqrtf(6.0f / (float)(h + a));
+  else lim = 0.0f;
+  return lim == 0.0f ? 0.0f : fma32(u, lim + lim, -lim);
+}
+
+// Genes 4 blk .. 4 blk + 3 of policy offspring j.
+template <bool GEN0>
+__device__ __forceinline__ float4 mlp_gene_block(const Params& p, const Pair& q, uint32_t g, int j,
+                                                 int blk) {
+  if (GEN0) {
+    const uint4 x = philox((uint32_t)blk, (uint32_t)j, 0u, kTagInit, p.key);
+    const int i = 4 * blk;
+    return make_float4(mlp_init_gene(p, i, unit24(x.x)), mlp_init_gene(p, i + 1, unit24(x.y)),
+                       mlp_init_gene(p, i + 2, unit24(x.z)), mlp_init_gene(p, i + 3, unit24(x.w)));
+  }
+  return make_genes<false>(p, q, g, j, 4 * blk);
+}
+
+__device__ __forceinline__ float pick4(const float4& v, int k) {
+  return k == 0 ? v.x : (k == 1 ? v.y : (k == 2 ? v.z : v.w));
+}
+
+// Fills dst[0 .. LEN) with genes first .. first+LEN-1, first a multiple of 4.
+template <bool GEN0, int LEN>
+__device__ __forceinline__ void mlp_genes_aligned(const Params& p, const Pair& q, uint32_t g,
+                                                  int j, int first, float* dst) {
+  static_assert(LEN % 4 == 0, "aligned runs hold whole gene blocks");
+#pragma unroll
+  for (int t4 = 0; t4 < LEN / 4; ++t4) {
+    const float4 v = mlp_gene_block<GEN0>(p, q, g, j, (first >> 2) + t4);
+    dst[4 * t4] = v.x;
+    dst[4 * t4 + 1] = v.y;
+    dst[4 * t4 + 2] = v.z;
+    dst[4 * t4 + 3] = v.w;
+  }
+}
+
+// Fills dst[0 .. LEN) with genes first .. first+LEN-1 (any alignment).
+template <bool GEN0, int LEN>
+__device__ __forceinline__ void mlp_genes_run(const Params& p, const Pair& q, uint32_t g, int j,
+                                              int first, float* dst) {
+  const int b0 = first >> 2, b1 = (first + LEN - 1) >> 2;
+  for (int blk = b0; blk <= b1; ++blk) {
+    const float4 v = mlp_gene_block<GEN0>(p, q, g, j, blk);
+#pragma unroll
+    for (int t = 0; t < LEN; ++t) {
+      const int gi = first + t;
+      if ((gi >> 2) == blk) dst[t] = pick4(v, gi & 3);
+    }
+  }
+}
+
+template <int H, bool GEN0, bool KEEP>
+__global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
+  constexpr int O = kObs, A = kAct;
+  constexpr int E1 = H * O, E2 = E1 + H, E3 = E2 + H * H, E4 = E3 + H;   // W3 at E4, b3 at E4 + A*H
+  __shared__ float s_state[2][32];
+  __shared__ float s_h1[H];
+  __shared__ float s_h2[H];
+  __shared__ float s_a[A];
+  __shared__ float s_w3[A][H];
+  __shared__ float s_b3[A];
+
+  const int o = threadIdx.x;
+  const int j = blockIdx.x;
+
+  Pair q{nullptr, nullptr, 0.0f, -1, -1};
+  if (!GEN0) {
+    const int nocc = p.counters[0];
+    if (nocc <= 0) {
+      if (o == 0) {
+        p.off_fit[j] = __builtin_nanf("");
+        p.off_par[2 * j] = -1;
+        p.off_par[2 * j + 1] = -1;
+        p.off_won[j] = 0;
+        atomicOr(reinterpret_cast<unsigned int*>(p.counters + 1), 1u);
+      }
+      return;
+    }
+    q = select_pair(p, g, j, nocc);
+  }
+
+  // ---- prologue: this individual's genotype, straight into registers / LDS
+  float w1[O], w2[H], arow[O], brow[A];
+  float b1v, b2v;
+  mlp_genes_run<GEN0, O>(p, q, g, j, o * O, w1);
+  mlp_genes_aligned<GEN0, H>(p, q, g, j, E2 + o * H, w2);   // E2 = 28 H
+  {
+    float t[1];
+    mlp_genes_run<GEN0, 1>(p, q, g, j, E1 + o, t);
+    b1v = t[0];
+    mlp_genes_run<GEN0, 1>(p, q, g, j, E3 + o, t);
+    b2v = t[0];
+  }
+  // W3 (A x H) and b3 (A): blocks shared out over the workgroup
+  for (int blk = (E4 >> 2) + o; blk < ((E4 + A * H + A) >> 2); blk += H) {
+    const float4 v = mlp_gene_block<GEN0>(p, q, g, j, blk);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int gi = 4 * blk + t - E4;
+      if (gi < A * H) s_w3[gi / H][gi % H] = pick4(v, t);
+      else s_b3[gi - A * H] = pick4(v, t);
+    }
+  }
+  if (KEEP) {
+    float* row = p.off_geno + (size_t)j * (size_t)p.stride;
+    for (int t = 0; t < O; ++t) row[o * O + t] = w1[t];
+    for (int t = 0; t < H; ++t) row[E2 + o * H + t] = w2[t];
+    row[E1 + o] = b1v;
+    row[E3 + o] = b2v;
+  }
+  const float* envA = p.env;
+  const float* envB = p.env + O * O;
+  const float* envS = p.env + O * O + O * A;
+  if (o < O) {
+#pragma unroll
+    for (int k = 0; k < O; ++k) arow[k] = envA[o * O + k];
+#pragma unroll
+    for (int k = 0; k < A; ++k) brow[k] = envB[o * A + k];
+    s_state[0][o] = envS[o];
+  }
+  __syncthreads();
+  if (KEEP) {
+    float* row = p.off_geno + (size_t)j * (size_t)p.stride;
+    for (int t = o; t < A * H; t += H) row[E4 + t] = s_w3[t / H][t % H];
+    if (o < A) row[E4 + A * H + o] = s_b3[o];
+  }
+
+  // ---- episode
+  float ret = 0.0f, dsum = 0.0f;
+  int cur = 0;
+  for (int step = 0; step < p.T; ++step) {
+    const float* s = s_state[cur];
+    float acc = b1v;
+#pragma unroll
+    for (int k = 0; k < O; ++k) acc = fma32(w1[k], s[k], acc);
+    s_h1[o] = tanh32(acc);
+    __syncthreads();
+    acc = b2v;
+#pragma unroll
+    for (int k = 0; k < H; ++k) acc = fma32(w2[k], s_h1[k], acc);
+    s_h2[o] = tanh32(acc);
+    __syncthreads();
+    if (o < A) {
+      acc = s_b3[o];
+#pragma unroll
+      for (int k = 0; k < H; ++k) acc = fma32(s_w3[o][k], s_h2[k], acc);
+      s_a[o] = tanh32(acc);
+    }
+    __syncthreads();
+    if (o < O) {
+      acc = 0.0f;
+#pragma unroll
+      for (int k = 0; k < O; ++k) acc = fma32(arow[k], s[k], acc);
+#pragma unroll
+      for (int k = 0; k < A; ++k) acc = fma32(brow[k], s_a[k], acc);
+      const float sn = tanh32(acc);
+      s_state[cur ^ 1][o] = sn;
+      if (o == 0) {
+        float qa = 0.0f;
+#pragma unroll
+        for (int k = 0; k < A; ++k) qa = fma32(s_a[k], s_a[k], qa);
+        ret = ret + fma32(-0.5f, qa, sn);
+      } else if (o <= 4) {
+        dsum = dsum + sigmoid32(sn);
+      }
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+  if (o == 0) {
+    p.off_fit[j] = ret;
+    p.off_par[2 * j] = q.c1;
+    p.off_par[2 * j + 1] = q.c2;
+    p.off_won[j] = 0;
+  } else if (o <= 4) {
+    p.off_desc[(size_t)j * 4 + (o - 1)] = dsum / (float)p.T;
+  }
+}
+
+// Winners of a policy batch: one wave per cell writes the winning offspring's
+// genotype into the cell's other bank (same gene formula as the prologue).
+template <bool GEN0>
+__global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (c >= p.C) return;
+  const uint64_t key = p.arch_key[c];
+  const uint32_t low = (uint32_t)key;
+  if (key == 0ull || low == 0xffffffffu) return;
+  const int j = p.nb - 1 - (int)low;
+  Pair q{nullptr, nullptr, 0.0f, -1, -1};
+  if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
+  float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
+  const int nblk = (p.n + 3) >> 2;
+  for (int blk = lane; blk < nblk; blk += 64)
+    *reinterpret_cast<float4*>(dst + 4 * blk) = mlp_gene_block<GEN0>(p, q, g, j, blk);
+  if (lane == 0) {
+    p.arch_fit[c] = p.off_fit[j];
+    for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
+    p.off_won[j] = 1;
+  }
+}
+
+inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hipStream_t s) {
+  const dim3 grid((unsigned)p.nb);
+#define QD_RO(H)                                                                                \
+  do {                                                                                          \
+    if (gen0) {                                                                                 \
+      if (keep) hipLaunchKernelGGL((k_rollout<H, true, true>), grid, dim3(H), 0, s, p, g);      \
+      else hipLaunchKernelGGL((k_rollout<H, true, false>), grid, dim3(H), 0, s, p, g);          \
+    } else {                                                                                    \
+      if (keep) hipLaunchKernelGGL((k_rollout<H, false, true>), grid, dim3(H), 0, s, p, g);     \
+      else hipLaunchKernelGGL((k_rollout<H, false, false>), grid, dim3(H), 0, s, p, g);         \
+    }                                                                                           \
+  } while (0)
+  if (p.hid == 64) QD_RO(64);
+  else QD_RO(128);
+#undef QD_RO
+}
+
+inline void launch_mlp_regen(const Params& p, bool gen0, uint32_t g, hipStream_t s) {
+  const dim3 grid((unsigned)((p.C + 3) / 4)), block(256);
+  if (gen0) hipLaunchKernelGGL((k_regen_mlp<true>), grid, block, 0, s, p, g);
+  else hipLaunchKernelGGL((k_regen_mlp<false>), grid, block, 0, s, p, g);
+}
+
+}  // namespace qd

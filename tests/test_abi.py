@@ -1,0 +1,124 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+validates configurations and workspaces before any GPU work."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2202_01258_amd import qd as Q
+from paper_2202_01258_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(Q.LIB_PATH):
+        pytest.skip("libqd.so not built")
+    return Q.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    header = open(os.path.join(ROOT, "include", "qd.h")).read()
+    declared = set(re.findall(r"^\s*(?:const char\*|qd_status)\s+(qd_\w+)\s*\(", header, re.M))
+    assert declared == set(Q.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name)
+
+
+def test_struct_layouts_match_the_header(lib, tmp_path):
+    """The ctypes mirrors have the C compiler's sizes and offsets."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = tmp_path / "sz.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "qd.h"\n'
+        'int main(void){printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(qd_config), '
+        'offsetof(qd_config, seed), offsetof(qd_config, keep_offspring), sizeof(qd_layout), '
+        'offsetof(qd_layout, row_stride), sizeof(qd_stats)); return 0;}\n')
+    exe = tmp_path / "sz"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    got = [int(t) for t in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    assert got == [C.sizeof(Q.QdConfig), Q.QdConfig.seed.offset,
+                   Q.QdConfig.keep_offspring.offset, C.sizeof(Q.QdLayout),
+                   Q.QdLayout.row_stride.offset, C.sizeof(Q.QdStats)]
+
+
+@pytest.mark.parametrize("name", W.ORDER)
+def test_layouts(lib, name):
+    w = W.workload(name)
+    lay = Q.layout_query(Q.make_config(w))
+    n = W.genotype_len(w)
+    assert lay.genotype_dim == n
+    assert lay.row_stride % 64 == 0 and lay.row_stride >= n
+    for b in range(Q.NUM_BUFFERS):
+        assert lay.offset[b] % 256 == 0
+        if b + 1 < Q.NUM_BUFFERS:
+            assert lay.offset[b] + lay.bytes[b] <= lay.offset[b + 1]
+    assert lay.bytes[Q.BUF_ARCHIVE_GENO] == 2 * w["C"] * lay.row_stride * 4
+    assert lay.bytes[Q.BUF_OFF_GENO] == 0
+    assert lay.workspace_bytes >= lay.offset[Q.NUM_BUFFERS - 1] + lay.bytes[Q.NUM_BUFFERS - 1]
+    if w["tess"] == W.CVT:
+        assert lay.bucket_res ** w["D"] == lay.num_buckets <= w["C"]
+    keep = Q.layout_query(Q.make_config(w, keep_offspring=True))
+    assert keep.bytes[Q.BUF_OFF_GENO] == w["batch"] * lay.row_stride * 4
+
+
+def status_of(w, **cfg_over):
+    c = Q.make_config(w)
+    for k, v in cfg_over.items():
+        setattr(c, k, v)
+    lay = Q.QdLayout()
+    return Q.lib().qd_layout_query(C.byref(c), C.byref(lay))
+
+
+@pytest.mark.parametrize("over", [
+    dict(abi_version=99), dict(task=7), dict(tess=3), dict(batch_size=0), dict(num_cells=0),
+    dict(genotype_dim=1), dict(desc_dim=3), dict(keep_offspring=2),
+])
+def test_invalid_configs(lib, over):
+    assert status_of(W.workload("rastrigin_grid_b128"), **over) == Q.QD_ERR_INVALID_ARG
+
+
+def test_invalid_grid_and_box(lib):
+    w = W.workload("rastrigin_grid_b128", grid=(100, 99))
+    assert status_of(w) == Q.QD_ERR_INVALID_ARG
+    w = W.workload("rastrigin_grid_b128", lo=(1.0, -1.0), hi=(1.0, 1.0))
+    assert status_of(w) == Q.QD_ERR_INVALID_ARG
+    w = W.workload("rastrigin_grid_b128", init_lo=0.5, init_hi=0.5)
+    assert status_of(w) == Q.QD_ERR_INVALID_ARG
+    w = W.workload("mlp64_cvt_b8192")
+    assert status_of(w, genotype_dim=6472) == Q.QD_ERR_INVALID_ARG
+    assert status_of(w, desc_dim=2) == Q.QD_ERR_INVALID_ARG
+    assert status_of(w, mlp_hidden=96) == Q.QD_ERR_UNSUPPORTED
+
+
+def test_workspace_checks_happen_before_gpu_work(lib):
+    w = W.workload("rastrigin_grid_b128")
+    c = Q.make_config(w)
+    lay = Q.layout_query(c)
+    h = C.c_void_p()
+    fake = C.c_void_p(1 << 40)          # never dereferenced: checks come first
+    st = lib.qd_archive_init(C.byref(c), fake, lay.workspace_bytes - 1, None, C.byref(h))
+    assert st == Q.QD_ERR_WORKSPACE_TOO_SMALL and not h.value
+    st = lib.qd_archive_init(C.byref(c), C.c_void_p((1 << 40) + 16), lay.workspace_bytes, None,
+                             C.byref(h))
+    assert st == Q.QD_ERR_INVALID_ARG
+    st = lib.qd_archive_init(C.byref(c), None, lay.workspace_bytes, None, C.byref(h))
+    assert st == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_generation(None, 1, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_archive_destroy(None) == Q.QD_OK
+    assert Q.status_str(Q.QD_ERR_WORKSPACE_TOO_SMALL) == "workspace too small"
+
+
+def test_product_path_refuses_without_gpu(lib):
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(RuntimeError):
+        Q.Archive(W.workload("rastrigin_grid_b128"))
