@@ -118,9 +118,10 @@ def main():
     stream.synchronize()
     log(f"bench: {args.warmup} warmup steps done; timing {args.steps} steps")
 
+    dominant = "rollout" if w["task"] == 3 else "vary_eval"
     if not args.no_kernel_timing:
-        a.set_kernel_timing(True)
-        a.kernel_times()          # clear
+        a.set_kernel_timing([dominant])     # events around the dominant kernel only
+        a.kernel_times()                    # clear
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -134,7 +135,16 @@ def main():
     wall = t1 - t0
     step_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
     ktimes = a.kernel_times() if not args.no_kernel_timing else {}
-    a.set_kernel_timing(False)
+    # every kernel, in a separate pass of the same length (events between all
+    # launches cost a few microseconds each, so they stay out of the timed steps)
+    breakdown = {}
+    if not args.no_kernel_timing:
+        a.set_kernel_timing(["vary_eval", "rollout", "cell_insert", "regen", "finalize"])
+        for _ in range(args.steps):
+            a.generation(g)
+            g += 1
+        breakdown = a.kernel_times()
+    a.set_kernel_timing([])
     st = a.stats()
     log(f"bench: timed region {wall * 1e3:.2f} ms; coverage {st['num_occupied']} cells")
 
@@ -159,9 +169,10 @@ def main():
     }
     gen_bytes = bytes_model["generation"] * nb
     line["generation_hbm_frac"] = gen_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9)
-    if ktimes:
+    if breakdown:
         line["kernel_ms_per_step"] = {k: (v[0] / v[1] if v[1] else 0.0)
-                                      for k, v in ktimes.items() if v[1]}
+                                      for k, v in breakdown.items() if v[1]}
+    if ktimes:
         if w["task"] == 3:
             ms, cnt = ktimes["rollout"]
             avg = ms / cnt

@@ -153,14 +153,23 @@ qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_sta
 /* The layout the handle was created with. */
 qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
 
-/* Turns per-kernel timing on or off.  When on, every launch is bracketed by
- * HIP events on the launch stream. */
-qd_status qd_set_kernel_timing(qd_archive* h, int32_t enable);
+/* Selects the kernels whose launches are bracketed by HIP events on the launch
+ * stream: bit k of kernel_mask is kernel QD_K_k (0 = no timing, the default).
+ * QD_ERR_INVALID_ARG for bits beyond QD_NUM_KERNELS. */
+qd_status qd_set_kernel_timing(qd_archive* h, uint32_t kernel_mask);
 
 /* Waits for the recorded events and returns, per QD_K_* kernel, the summed
  * duration in ms and the number of launches since the last call; then clears
  * them.  ms and counts must hold QD_NUM_KERNELS entries. */
 qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts);
+
+/* Self-check of the short division and square-root sequences the Box-Muller
+ * sampler uses in place of IEEE division and square root: for every one of the
+ * 2^24 possible radius inputs, compares the two and stores the number of
+ * differing results in *mismatches (0 means the sampler's output equals the
+ * IEEE-arithmetic definition bit for bit).  d_scratch: 8 bytes of device
+ * memory owned by the caller, 8-byte aligned.  Synchronises `stream`. */
+qd_status qd_check_fast_arith(void* d_scratch, void* stream, uint64_t* mismatches);
 
 /* Frees the host handle (not the workspace).  NULL is accepted. */
 qd_status qd_archive_destroy(qd_archive* h);

@@ -24,6 +24,11 @@ struct Key {
   uint32_t k0, k1;
 };
 
+// a ^ b ^ c in one v_bitop3_b32 (truth table 0x96)
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                         Key key) {
   uint32_t k0 = key.k0, k1 = key.k1;
@@ -31,8 +36,8 @@ __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
   for (int round = 0; round < 10; ++round) {
     const uint64_t m0 = (uint64_t)0xD2511F53u * c0;   // one v_mad_u64_u32 each
     const uint64_t m1 = (uint64_t)0xCD9E8D57u * c2;
-    const uint32_t n0 = (uint32_t)(m1 >> 32) ^ c1 ^ k0;
-    const uint32_t n2 = (uint32_t)(m0 >> 32) ^ c3 ^ k1;
+    const uint32_t n0 = xor3((uint32_t)(m1 >> 32), c1, k0);
+    const uint32_t n2 = xor3((uint32_t)(m0 >> 32), c3, k1);
     c0 = n0;
     c1 = (uint32_t)m1;
     c2 = n2;
@@ -63,15 +68,41 @@ constexpr float kPi = 0x1.921fb6p+1f;
 constexpr float kHalfPi = 0x1.921fb6p+0f;
 constexpr float kLog2e = 0x1.715476p+0f;
 
+// Quotient a / b for b in [1.7, 2.5] (so no scaling is ever needed):
+// hardware reciprocal, product, one residual correction.  On the inputs the
+// logarithm below can see it returns the IEEE quotient bit for bit; the library
+// checks that over all of them (qd_check_fast_arith).
+__device__ __forceinline__ float div_narrow(float a, float b) {
+  const float y = __builtin_amdgcn_rcpf(b);
+  const float q = a * y;
+  const float r = fma32(-q, b, a);
+  return fma32(r, y, q);
+}
+
+// Square root of a positive normal x (or +-0) without the small-input
+// scaling: hardware estimate, then the neighbour one unit in the last place
+// below or above is taken when the fma residual says the estimate rounded
+// the wrong way.  Checked against IEEE sqrt like div_narrow.
+__device__ __forceinline__ float sqrt_normal(float x) {
+  const float s = __builtin_amdgcn_sqrtf(x);
+  const float dn = __uint_as_float(__float_as_uint(s) - 1u);
+  const float up = __uint_as_float(__float_as_uint(s) + 1u);
+  float r = fma32(-dn, s, x) <= 0.0f ? dn : s;
+  r = fma32(-up, s, x) > 0.0f ? up : r;
+  return x == 0.0f ? x : r;
+}
+
 // ln x for positive normal x.  x = 2^e m, m folded into [sqrt(1/2), sqrt(2));
 // ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd series through s^9.
+// FAST selects div_narrow for the quotient; both give the same bits.
+template <bool FAST = false>
 __device__ __forceinline__ float log_pos(float x) {
   const uint32_t bits = __float_as_uint(x);
   const uint32_t frac = bits & 0x7fffffu;
   const bool fold = frac > 0x3504f3u;
   const int e = (int)(bits >> 23) - 127 + (fold ? 1 : 0);
   const float m = __uint_as_float((frac | 0x3f800000u) - (fold ? 0x00800000u : 0u));
-  const float s = (m - 1.0f) / (m + 1.0f);
+  const float s = FAST ? div_narrow(m - 1.0f, m + 1.0f) : (m - 1.0f) / (m + 1.0f);
   const float s2 = s * s;
   float p = fma32(s2, 2.0f / 9.0f, 2.0f / 7.0f);
   p = fma32(s2, p, 2.0f / 5.0f);
@@ -106,17 +137,27 @@ __device__ __forceinline__ float2 turn_cos_sin(uint32_t m) {
   const float f = (float)((int32_t)m - (int32_t)(q << 22)) * 0x1p-22f;
   const float x = f * kHalfPi;
   const float s = sin_small(x), c = cos_small(x);
-  switch (q & 3u) {
-    case 0: return make_float2(c, s);
-    case 1: return make_float2(-s, c);
-    case 2: return make_float2(-c, -s);
-    default: return make_float2(s, -c);
-  }
+  // quarter turns q = 0..3 (4 = 0): (c, s), (-s, c), (-c, -s), (s, -c),
+  // written as a swap on odd q and sign flips, without branches
+  const bool odd = (q & 1u) != 0u;
+  const float a = odd ? s : c, b = odd ? c : s;
+  const uint32_t flip_cos = ((q + 1u) & 2u) << 30, flip_sin = (q & 2u) << 30;
+  return make_float2(__uint_as_float(__float_as_uint(a) ^ flip_cos),
+                     __uint_as_float(__float_as_uint(b) ^ flip_sin));
+}
+
+// Box-Muller radius sqrt(-2 ln u1), u1 the (0,1] uniform of word xa: with
+// IEEE division and square root, and with the short sequences (FAST).
+__device__ __forceinline__ float bm_radius_ieee(uint32_t xa) {
+  return __builtin_sqrtf(-2.0f * log_pos<false>(unit24_open0(xa)));
+}
+__device__ __forceinline__ float bm_radius(uint32_t xa) {
+  return sqrt_normal(-2.0f * log_pos<true>(unit24_open0(xa)));
 }
 
 // Two standard normals (Box-Muller) from two Philox words.
 __device__ __forceinline__ float2 gauss2(uint32_t xa, uint32_t xb) {
-  const float r = __builtin_sqrtf(-2.0f * log_pos(unit24_open0(xa)));
+  const float r = bm_radius(xa);
   const float2 cs = turn_cos_sin(xb >> 8);
   return make_float2(r * cs.x, r * cs.y);
 }

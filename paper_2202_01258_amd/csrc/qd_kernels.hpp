@@ -109,8 +109,9 @@ __device__ __forceinline__ float4 make_genes(const Params& p, const Pair& q, uin
   }
 }
 
+// min(max(x, lo), hi) for lo < hi and x not NaN, in one v_med3_f32.
 __device__ __forceinline__ float clip(float x, float lo, float hi) {
-  return __builtin_fminf(__builtin_fmaxf(x, lo), hi);
+  return __builtin_amdgcn_fmed3f(x, lo, hi);
 }
 
 template <int TASK>
@@ -156,19 +157,48 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   for (int base = 4 * lane; base < n; base += 256) {
     const float4 v4 = make_genes<GEN0>(p, q, g, j, base);
     if (KEEP) *reinterpret_cast<float4*>(keep_row + base) = v4;
-    const float v[4] = {v4.x, v4.y, v4.z, v4.w};
     if (base == 0) {
-      g0 = v[0];
-      g1 = v[1];
+      g0 = v4.x;
+      g1 = v4.y;
     }
+    if (base + 4 <= n) {
+      // whole block: the same additions in the same order, without per-gene tests
+      acc = acc + task_term<TASK>(v4.x);
+      acc = acc + task_term<TASK>(v4.y);
+      acc = acc + task_term<TASK>(v4.z);
+      acc = acc + task_term<TASK>(v4.w);
+      if (TASK == kTaskProj) {
+        if (base + 4 <= half) {
+          dlo = dlo + clip(v4.x, p.lo[0], p.hi[0]);
+          dlo = dlo + clip(v4.y, p.lo[0], p.hi[0]);
+          dlo = dlo + clip(v4.z, p.lo[0], p.hi[0]);
+          dlo = dlo + clip(v4.w, p.lo[0], p.hi[0]);
+        } else if (base >= half) {
+          dhi = dhi + clip(v4.x, p.lo[1], p.hi[1]);
+          dhi = dhi + clip(v4.y, p.lo[1], p.hi[1]);
+          dhi = dhi + clip(v4.z, p.lo[1], p.hi[1]);
+          dhi = dhi + clip(v4.w, p.lo[1], p.hi[1]);
+        } else {
+          const float v[4] = {v4.x, v4.y, v4.z, v4.w};
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int gi = base + k;
-      if (gi < n) {
-        acc = acc + task_term<TASK>(v[k]);
-        if (TASK == kTaskProj) {
-          if (gi < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
-          else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+          for (int k = 0; k < 4; ++k) {
+            if (base + k < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
+            else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+          }
+        }
+      }
+    } else {
+      // ragged last block
+      const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int gi = base + k;
+        if (gi < n) {
+          acc = acc + task_term<TASK>(v[k]);
+          if (TASK == kTaskProj) {
+            if (gi < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
+            else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+          }
         }
       }
     }
@@ -213,10 +243,33 @@ __device__ __forceinline__ int grid_cell(const Params& p, const float* d) {
 // Chebyshev order until the best distance found is certainly below the
 // distance to every unvisited bucket (with a relative margin far above the
 // fp32 rounding of either side), so the answer equals the brute-force argmin.
+template <int D>
+__device__ __forceinline__ void visit_bucket(const Params& p, int bucket, const float* u,
+                                             float& best, int& best_idx) {
+  const int s0 = p.bucket_start[bucket], s1 = p.bucket_start[bucket + 1];
+  for (int s = s0; s < s1; ++s) {
+    const float4 c = p.bucket_pts[s];
+    const float cc[4] = {c.x, c.y, c.z, c.w};
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      const float diff = u[k] - cc[k];
+      acc = fma32(diff, diff, acc);
+    }
+    const int idx = p.bucket_idx[s];
+    if (acc < best || (acc == best && idx < best_idx)) {
+      best = acc;
+      best_idx = idx;
+    }
+  }
+}
+
+template <int D>
 __device__ int cvt_cell(const Params& p, const float* d) {
-  const int D = p.D, R = p.bucket_res;
-  float u[4];
-  int qb[4];
+  const int R = p.bucket_res;
+  float u[D];
+  int qb[D];
+#pragma unroll
   for (int k = 0; k < D; ++k) {
     if (!(d[k] == d[k])) return -1;
     u[k] = (d[k] - p.lo[k]) / p.span[k];
@@ -228,41 +281,42 @@ __device__ int cvt_cell(const Params& p, const float* d) {
   int best_idx = 0x7fffffff;
   const double invR = 1.0 / (double)R;
   for (int r = 0; r < R; ++r) {
-    const int side = 2 * r + 1;
-    int span_n = 1;
-    for (int k = 0; k < D; ++k) span_n *= side;
-    for (int e = 0; e < span_n; ++e) {
-      int rest = e, bucket = 0, cheb = 0;
-      bool inside = true;
-      for (int k = 0; k < D; ++k) {
-        const int off = rest % side - r;
-        rest /= side;
-        const int b = qb[k] + off;
-        if (b < 0 || b >= R) inside = false;
-        const int a = off < 0 ? -off : off;
-        cheb = a > cheb ? a : cheb;
-        bucket = bucket * R + b;
-      }
-      if (!inside || cheb != r) continue;
-      const int s0 = p.bucket_start[bucket], s1 = p.bucket_start[bucket + 1];
-      for (int s = s0; s < s1; ++s) {
-        const float4 c = p.bucket_pts[s];
-        const float cc[4] = {c.x, c.y, c.z, c.w};
-        float acc = 0.0f;
-        for (int k = 0; k < D; ++k) {
-          const float diff = u[k] - cc[k];
-          acc = fma32(diff, diff, acc);
+    // buckets at Chebyshev distance exactly r, in range
+    if (D == 2) {
+      for (int o0 = -r; o0 <= r; ++o0) {
+        const int b0 = qb[0] + o0;
+        if (b0 < 0 || b0 >= R) continue;
+        const int step = (o0 == -r || o0 == r) ? 1 : 2 * r;
+        for (int o1 = -r; o1 <= r; o1 += step) {
+          const int b1 = qb[1] + o1;
+          if (b1 >= 0 && b1 < R) visit_bucket<D>(p, b0 * R + b1, u, best, best_idx);
         }
-        const int idx = p.bucket_idx[s];
-        if (acc < best || (acc == best && idx < best_idx)) {
-          best = acc;
-          best_idx = idx;
+      }
+    } else {
+      for (int o0 = -r; o0 <= r; ++o0) {
+        const int b0 = qb[0] + o0;
+        if (b0 < 0 || b0 >= R) continue;
+        for (int o1 = -r; o1 <= r; ++o1) {
+          const int b1 = qb[1] + o1;
+          if (b1 < 0 || b1 >= R) continue;
+          for (int o2 = -r; o2 <= r; ++o2) {
+            const int b2 = qb[2] + o2;
+            if (b2 < 0 || b2 >= R) continue;
+            const bool edge = o0 == -r || o0 == r || o1 == -r || o1 == r || o2 == -r || o2 == r;
+            const int step = edge ? 1 : (r == 0 ? 1 : 2 * r);
+            for (int o3 = -r; o3 <= r; o3 += step) {
+              const int b3 = qb[3] + o3;
+              if (b3 >= 0 && b3 < R)
+                visit_bucket<D>(p, ((b0 * R + b1) * R + b2) * R + b3, u, best, best_idx);
+            }
+          }
         }
       }
     }
     // lower bound on the distance to anything outside the visited box
     double bound = __builtin_inf();
     bool face = false;
+#pragma unroll
     for (int k = 0; k < D; ++k) {
       if (qb[k] - r >= 1) {
         const double gap = (double)u[k] - (double)(qb[k] - r) * invR - 1e-6;
@@ -281,24 +335,36 @@ __device__ int cvt_cell(const Params& p, const float* d) {
   return best_idx;
 }
 
-template <int TESS>
-__global__ __launch_bounds__(256) void k_cell_insert(const Params p) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
+// Cell of each offspring, then insertion by packed-key maximum.  Keys are
+// folded per wave (lanes sharing a cell), then per workgroup in an LDS hash
+// table, so each workgroup issues one global 64-bit atomicMax per distinct
+// cell it saw -- a batch crowding into a few cells does not serialise on them.
+constexpr int kInsertBlock = 256, kInsertSlots = 512;
+
+template <int TESS, int D>
+__global__ __launch_bounds__(kInsertBlock) void k_cell_insert(const Params p) {
+  __shared__ int tag[kInsertSlots];
+  __shared__ unsigned long long kmax[kInsertSlots];
+  for (int e = threadIdx.x; e < kInsertSlots; e += kInsertBlock) {
+    tag[e] = -1;
+    kmax[e] = 0ull;
+  }
+  __syncthreads();
+  const int j = blockIdx.x * kInsertBlock + threadIdx.x;
   int cell = -1;
   uint64_t key = 0;
   if (j < p.nb) {
     const float f = p.off_fit[j];
     if (f == f) {
-      float d[4];
-      for (int k = 0; k < p.D; ++k) d[k] = p.off_desc[(size_t)j * p.D + k];
-      cell = TESS == kTessGrid ? grid_cell(p, d) : cvt_cell(p, d);
+      float d[D];
+#pragma unroll
+      for (int k = 0; k < D; ++k) d[k] = p.off_desc[(size_t)j * D + k];
+      cell = TESS == kTessGrid ? grid_cell(p, d) : cvt_cell<D>(p, d);
     }
     p.off_cell[j] = cell;
     if (cell >= 0)
       key = ((uint64_t)order_bits(f) << 32) | (uint64_t)(uint32_t)(p.nb - 1 - j);
   }
-  // one atomic per distinct cell per wave: the lanes that share the leader's
-  // cell fold their keys with max, the leader issues the atomic.
   uint64_t todo = __ballot(cell >= 0);
   while (todo) {
     const int leader = __ffsll((unsigned long long)todo) - 1;
@@ -310,8 +376,23 @@ __global__ __launch_bounds__(256) void k_cell_insert(const Params p) {
       const uint64_t o = __shfl_xor(k, h, 64);
       k = o > k ? o : k;
     }
-    if (lane_id() == leader) atomicMax((unsigned long long*)&p.arch_key[c], (unsigned long long)k);
+    if (lane_id() == leader) {
+      int h = (int)(((uint32_t)c * 2654435761u) >> 23) & (kInsertSlots - 1);
+      for (;;) {   // at most kInsertBlock distinct cells: a free slot always exists
+        const int t = atomicCAS(&tag[h], -1, c);
+        if (t == -1 || t == c) {
+          atomicMax(&kmax[h], (unsigned long long)k);
+          break;
+        }
+        h = (h + 1) & (kInsertSlots - 1);
+      }
+    }
     todo &= ~same;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < kInsertSlots; e += kInsertBlock) {
+    const int c = tag[e];
+    if (c >= 0) atomicMax((unsigned long long*)&p.arch_key[c], kmax[e]);
   }
 }
 
@@ -319,24 +400,27 @@ __global__ __launch_bounds__(256) void k_cell_insert(const Params p) {
 // Winners: one wave per cell regenerates the winning offspring's genotype into
 // the cell's other bank and records its objective and descriptor.
 // ---------------------------------------------------------------------------
+constexpr int kRegenCellsPerWave = 8;
+
 template <bool GEN0>
 __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
   const int lane = threadIdx.x & 63;
-  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (c >= p.C) return;
-  const uint64_t key = p.arch_key[c];
-  const uint32_t low = (uint32_t)key;
-  if (key == 0ull || low == 0xffffffffu) return;
-  const int j = p.nb - 1 - (int)low;
-  Pair q{nullptr, nullptr, 0.0f, -1, -1};
-  if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
-  float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
-  for (int base = 4 * lane; base < p.n; base += 256)
-    *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
-  if (lane == 0) {
-    p.arch_fit[c] = p.off_fit[j];
-    for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
-    p.off_won[j] = 1;
+  const int first = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kRegenCellsPerWave;
+  for (int c = first; c < first + kRegenCellsPerWave && c < p.C; ++c) {
+    const uint64_t key = p.arch_key[c];
+    const uint32_t low = (uint32_t)key;
+    if (key == 0ull || low == 0xffffffffu) continue;
+    const int j = p.nb - 1 - (int)low;
+    Pair q{nullptr, nullptr, 0.0f, -1, -1};
+    if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
+    float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
+    for (int base = 4 * lane; base < p.n; base += 256)
+      *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
+    if (lane == 0) {
+      p.arch_fit[c] = p.off_fit[j];
+      for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
+      p.off_won[j] = 1;
+    }
   }
 }
 
@@ -345,36 +429,47 @@ __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
 // so a later offspring needs a strictly greater objective); then the filled
 // cells are compacted in ascending order.  One workgroup of 1024 threads.
 // ---------------------------------------------------------------------------
+constexpr int kFinalizeItems = 16;
+
 __global__ __launch_bounds__(1024) void k_finalize(const Params p) {
-  __shared__ int wave_cnt[16];
+  __shared__ int wave_tot[16];
   __shared__ int base_sh;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) base_sh = 0;
-  __syncthreads();
-  for (int start = 0; start < p.C; start += 1024) {
-    const int c = start + tid;
-    bool filled = false;
-    if (c < p.C) {
-      const uint64_t key = p.arch_key[c];
-      if (key != 0ull) {
-        filled = true;
-        if ((uint32_t)key != 0xffffffffu) {
-          p.arch_slot[c] ^= 1u;
-          p.arch_key[c] = key | 0xffffffffull;
+  for (int start = 0; start < p.C; start += 1024 * kFinalizeItems) {
+    // each thread owns kFinalizeItems consecutive cells; all loads first
+    const int c0 = start + tid * kFinalizeItems;
+    uint64_t keys[kFinalizeItems];
+#pragma unroll
+    for (int i = 0; i < kFinalizeItems; ++i) keys[i] = c0 + i < p.C ? p.arch_key[c0 + i] : 0ull;
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kFinalizeItems; ++i) {
+      if (keys[i] != 0ull) {
+        ++cnt;
+        if ((uint32_t)keys[i] != 0xffffffffu) {
+          p.arch_slot[c0 + i] ^= 1u;
+          p.arch_key[c0 + i] = keys[i] | 0xffffffffull;
         }
       }
     }
-    const uint64_t bal = __ballot(filled);
-    const int below = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) wave_cnt[wave] = __popcll(bal);
+    int incl = cnt;
+#pragma unroll
+    for (int h = 1; h < 64; h <<= 1) {
+      const int o = __shfl_up(incl, h, 64);
+      if (lane >= h) incl += o;
+    }
+    if (lane == 63) wave_tot[wave] = incl;
     __syncthreads();
-    int off = base_sh;
-    for (int w = 0; w < wave; ++w) off += wave_cnt[w];
-    if (filled) p.occ_list[off + below] = c;
+    int off = base_sh + incl - cnt;
+    for (int w = 0; w < wave; ++w) off += wave_tot[w];
+#pragma unroll
+    for (int i = 0; i < kFinalizeItems; ++i)
+      if (keys[i] != 0ull) p.occ_list[off++] = c0 + i;
     __syncthreads();
     if (tid == 0) {
       int tot = 0;
-      for (int w = 0; w < 16; ++w) tot += wave_cnt[w];
+      for (int w = 0; w < 16; ++w) tot += wave_tot[w];
       base_sh += tot;
     }
     __syncthreads();
@@ -521,6 +616,18 @@ __global__ void k_env(const Params p, int count) {
   const float z[4] = {z01.x, z01.y, z23.x, z23.y};
   for (int k = 0; k < 4; ++k)
     if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
+}
+
+// Self-check of the short division / square-root sequences: the Box-Muller
+// radius for every one of the 2^24 possible 24-bit inputs, against the IEEE
+// operations.  Counts mismatches into *count.
+__global__ void k_zero_u64(unsigned long long* x) { *x = 0ull; }
+
+__global__ __launch_bounds__(256) void k_check_radius(unsigned long long* count) {
+  const uint32_t k = blockIdx.x * 256u + threadIdx.x;       // 0 .. 2^24 - 1
+  const uint32_t xa = k << 8;
+  const float a = bm_radius(xa), b = bm_radius_ieee(xa);
+  if (__float_as_uint(a) != __float_as_uint(b)) atomicAdd(count, 1ull);
 }
 
 }  // namespace qd

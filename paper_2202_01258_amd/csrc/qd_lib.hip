@@ -134,7 +134,7 @@ struct qd_archive {
   qd_config cfg;
   qd_layout lay;
   qd::Params p;
-  bool timing = false;
+  uint32_t timing_mask = 0;
   struct Rec {
     int kernel;
     hipEvent_t a, b;
@@ -168,13 +168,13 @@ struct Timed {
   int kernel;
   hipEvent_t a = nullptr;
   Timed(qd_archive* h_, hipStream_t s_, int k) : h(h_), s(s_), kernel(k) {
-    if (h->timing) {
+    if ((h->timing_mask >> kernel) & 1u) {
       a = take_event(h);
       if (a) (void)hipEventRecord(a, s);
     }
   }
   ~Timed() {
-    if (h->timing && a) {
+    if (a) {
       hipEvent_t b = take_event(h);
       if (b) {
         (void)hipEventRecord(b, s);
@@ -212,16 +212,21 @@ void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
 void launch_cell_insert(qd_archive* h, hipStream_t s) {
   const qd::Params& p = h->p;
   Timed t(h, s, QD_K_CELL_INSERT);
-  const dim3 grid(blocks_for((uint64_t)p.nb, 256)), block(256);
-  if (p.tess == qd::kTessGrid) hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessGrid>), grid, block, 0, s, p);
-  else hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessCvt>), grid, block, 0, s, p);
+  const dim3 grid(blocks_for((uint64_t)p.nb, qd::kInsertBlock)), block(qd::kInsertBlock);
+  if (p.tess == qd::kTessGrid) {
+    if (p.D == 2) hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessGrid, 2>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessGrid, 4>), grid, block, 0, s, p);
+  } else {
+    if (p.D == 2) hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessCvt, 2>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessCvt, 4>), grid, block, 0, s, p);
+  }
 }
 
 template <bool GEN0>
 void launch_regen(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
   Timed t(h, s, QD_K_REGEN);
-  const dim3 grid(blocks_for((uint64_t)p.C, 4)), block(256);
+  const dim3 grid(blocks_for((uint64_t)p.C, 4 * qd::kRegenCellsPerWave)), block(256);
   if (p.task == qd::kTaskMlp) qd::launch_mlp_regen(p, GEN0, g, s);
   else hipLaunchKernelGGL((qd::k_regen<GEN0>), grid, block, 0, s, p, g);
 }
@@ -384,9 +389,9 @@ qd_status qd_archive_layout(const qd_archive* h, qd_layout* out) {
   return QD_OK;
 }
 
-qd_status qd_set_kernel_timing(qd_archive* h, int32_t enable) {
-  if (!h) return QD_ERR_INVALID_ARG;
-  h->timing = enable != 0;
+qd_status qd_set_kernel_timing(qd_archive* h, uint32_t kernel_mask) {
+  if (!h || (kernel_mask >> QD_NUM_KERNELS) != 0u) return QD_ERR_INVALID_ARG;
+  h->timing_mask = kernel_mask;
   return QD_OK;
 }
 
@@ -409,6 +414,23 @@ qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts) {
   }
   h->recs.clear();
   return st;
+}
+
+qd_status qd_check_fast_arith(void* d_scratch, void* stream, uint64_t* mismatches) {
+  if (!d_scratch || !mismatches) return QD_ERR_INVALID_ARG;
+  if (((uintptr_t)d_scratch % 8) != 0) return QD_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  auto* count = (unsigned long long*)d_scratch;
+  hipLaunchKernelGGL(qd::k_zero_u64, dim3(1), dim3(1), 0, s, count);
+  hipLaunchKernelGGL(qd::k_check_radius, dim3(1u << 16), dim3(256), 0, s, count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e);
+  unsigned long long host = 0;
+  e = hipMemcpyAsync(&host, count, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e);
+  *mismatches = host;
+  return QD_OK;
 }
 
 qd_status qd_archive_destroy(qd_archive* h) {

@@ -220,22 +220,23 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
 template <bool GEN0>
 __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
   const int lane = threadIdx.x & 63;
-  const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (c >= p.C) return;
-  const uint64_t key = p.arch_key[c];
-  const uint32_t low = (uint32_t)key;
-  if (key == 0ull || low == 0xffffffffu) return;
-  const int j = p.nb - 1 - (int)low;
-  Pair q{nullptr, nullptr, 0.0f, -1, -1};
-  if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
-  float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
-  const int nblk = (p.n + 3) >> 2;
-  for (int blk = lane; blk < nblk; blk += 64)
-    *reinterpret_cast<float4*>(dst + 4 * blk) = mlp_gene_block<GEN0>(p, q, g, j, blk);
-  if (lane == 0) {
-    p.arch_fit[c] = p.off_fit[j];
-    for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
-    p.off_won[j] = 1;
+  const int first = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kRegenCellsPerWave;
+  for (int c = first; c < first + kRegenCellsPerWave && c < p.C; ++c) {
+    const uint64_t key = p.arch_key[c];
+    const uint32_t low = (uint32_t)key;
+    if (key == 0ull || low == 0xffffffffu) continue;
+    const int j = p.nb - 1 - (int)low;
+    Pair q{nullptr, nullptr, 0.0f, -1, -1};
+    if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
+    float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
+    const int nblk = (p.n + 3) >> 2;
+    for (int blk = lane; blk < nblk; blk += 64)
+      *reinterpret_cast<float4*>(dst + 4 * blk) = mlp_gene_block<GEN0>(p, q, g, j, blk);
+    if (lane == 0) {
+      p.arch_fit[c] = p.off_fit[j];
+      for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
+      p.off_won[j] = 1;
+    }
   }
 }
 
@@ -257,7 +258,8 @@ inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hi
 }
 
 inline void launch_mlp_regen(const Params& p, bool gen0, uint32_t g, hipStream_t s) {
-  const dim3 grid((unsigned)((p.C + 3) / 4)), block(256);
+  const dim3 grid((unsigned)((p.C + 4 * kRegenCellsPerWave - 1) / (4 * kRegenCellsPerWave))),
+      block(256);
   if (gen0) hipLaunchKernelGGL((k_regen_mlp<true>), grid, block, 0, s, p, g);
   else hipLaunchKernelGGL((k_regen_mlp<false>), grid, block, 0, s, p, g);
 }

@@ -30,7 +30,7 @@ KERNEL_NAMES = ["vary_eval", "rollout", "cell_insert", "regen", "finalize", "set
 # Every symbol include/qd.h declares.
 EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_archive_stats",
            "qd_archive_layout", "qd_set_kernel_timing", "qd_kernel_times",
-           "qd_archive_destroy", "qd_status_str"]
+           "qd_check_fast_arith", "qd_archive_destroy", "qd_status_str"]
 
 
 class QdConfig(C.Structure):
@@ -84,8 +84,9 @@ def lib():
         L.qd_generation.argtypes = [P, C.c_uint32, P]
         L.qd_archive_stats.argtypes = [P, C.c_double, P, C.POINTER(QdStats)]
         L.qd_archive_layout.argtypes = [P, C.POINTER(QdLayout)]
-        L.qd_set_kernel_timing.argtypes = [P, C.c_int32]
+        L.qd_set_kernel_timing.argtypes = [P, C.c_uint32]
         L.qd_kernel_times.argtypes = [P, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
+        L.qd_check_fast_arith.argtypes = [P, P, C.POINTER(C.c_uint64)]
         L.qd_archive_destroy.argtypes = [P]
         L.qd_status_str.argtypes = [S]
         L.qd_status_str.restype = C.c_char_p
@@ -127,6 +128,18 @@ def layout_query(cfg: QdConfig) -> QdLayout:
     out = QdLayout()
     _check(lib().qd_layout_query(C.byref(cfg), C.byref(out)), "qd_layout_query")
     return out
+
+
+def check_fast_arith(device: str = "cuda:0") -> int:
+    """Number of the 2^24 Box-Muller radius inputs where the short division /
+    square-root sequences differ from IEEE arithmetic (0 = identical)."""
+    import torch
+    scratch = torch.zeros(1, dtype=torch.int64, device=device)
+    out = C.c_uint64()
+    _check(lib().qd_check_fast_arith(C.c_void_p(scratch.data_ptr()),
+                                     C.c_void_p(_stream_handle(None)), C.byref(out)),
+           "qd_check_fast_arith")
+    return int(out.value)
 
 
 def _stream_handle(stream) -> int:
@@ -183,8 +196,12 @@ class Archive:
         return dict(qd_score=out.qd_score, coverage=out.coverage, best=out.best_fitness,
                     num_occupied=out.num_occupied, flags=out.flags)
 
-    def set_kernel_timing(self, on: bool):
-        _check(lib().qd_set_kernel_timing(self._h, 1 if on else 0), "qd_set_kernel_timing")
+    def set_kernel_timing(self, kernels=()):
+        """Time the launches of the named kernels (KERNEL_NAMES); () turns it off."""
+        mask = 0
+        for k in kernels:
+            mask |= 1 << KERNEL_NAMES.index(k)
+        _check(lib().qd_set_kernel_timing(self._h, mask), "qd_set_kernel_timing")
 
     def kernel_times(self) -> dict:
         ms = (C.c_double * NUM_KERNELS)()

@@ -271,3 +271,9 @@ def test_edge_shapes(kw):
         o.generation(g)
         np.testing.assert_array_equal(a.last_batch()["geno"], o.last_offspring())
     assert_archive_equal(a.snapshot(), o.archive(), o.n, f"{kw}")
+
+
+def test_fast_division_and_sqrt_equal_ieee_on_all_inputs():
+    """The Box-Muller radius uses short rcp/sqrt sequences; over all 2^24
+    inputs they must reproduce IEEE division and square root bit for bit."""
+    assert qd().check_fast_arith() == 0
