@@ -91,6 +91,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-generations", type=int, default=2)
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="also run 3 plain device-to-device copies of MIB MiB (the reference "
+                         "kernel for scaling HBM byte counters) and exit after them")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -104,6 +107,14 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        nbytes = args.copy_calibration << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: copied {nbytes} bytes 3 times (counter calibration)")
     w = W.workload(args.workload)
     n = W.genotype_len(w)
     nb = w["batch"]
@@ -139,7 +150,7 @@ def main():
     # launches cost a few microseconds each, so they stay out of the timed steps)
     breakdown = {}
     if not args.no_kernel_timing:
-        a.set_kernel_timing(["vary_eval", "rollout", "cell_insert", "regen", "finalize"])
+        a.set_kernel_timing(["vary_eval", "rollout", "insert", "regen"])
         for _ in range(args.steps):
             a.generation(g)
             g += 1

@@ -84,12 +84,14 @@ enum {
   QD_BUF_BUCKET_ITEMS,     /* f32x4 + i32: bucketed centroid copies and indices       */
   QD_BUF_ENV,              /* f32: A [obs][obs], B [obs][act], s0 [obs]               */
   QD_BUF_OCC_LIST,         /* i32 [C]   filled cells, ascending                       */
-  QD_BUF_COUNTERS,         /* i32 [64]  [0] = number of filled cells, [1] = flags     */
+  QD_BUF_COUNTERS,         /* i32 [64]  [0] filled cells, [1] flags, [3] internal     */
   QD_BUF_OFF_PARENTS,      /* i32 [N_B][2] parent cells of the last batch            */
   QD_BUF_OFF_FIT,          /* f32 [N_B]                                               */
   QD_BUF_OFF_DESC,         /* f32 [N_B][D]                                            */
   QD_BUF_OFF_CELL,         /* i32 [N_B] cell, -1 = invalid (never inserted)          */
   QD_BUF_OFF_WON,          /* u8  [N_B] 1 = holds its cell after the batch           */
+  QD_BUF_OFF_KEY,          /* u64 [N_B] insertion key (0 = not inserted)              */
+  QD_BUF_OFF_BANK,         /* u8  [N_B] genotype banks of parent 1 (bit 0), 2 (bit 1) */
   QD_BUF_OFF_GENO,         /* f32 [N_B][row_stride] (keep_offspring only)            */
   QD_BUF_STATS,            /* f64 [8]   device-side statistics                        */
   QD_NUM_BUFFERS
@@ -117,8 +119,8 @@ typedef struct {
 typedef struct qd_archive qd_archive;
 
 /* Kernels whose durations qd_kernel_times() reports. */
-enum { QD_K_VARY_EVAL = 0, QD_K_ROLLOUT, QD_K_CELL_INSERT, QD_K_REGEN, QD_K_FINALIZE,
-       QD_K_SETUP, QD_NUM_KERNELS };
+enum { QD_K_VARY_EVAL = 0, QD_K_ROLLOUT, QD_K_INSERT, QD_K_REGEN, QD_K_SETUP,
+       QD_NUM_KERNELS };
 
 /* Validates *cfg and fills *out with the workspace layout.  Host only; no GPU
  * work.  QD_ERR_INVALID_ARG for an inconsistent config (task/tessellation/D

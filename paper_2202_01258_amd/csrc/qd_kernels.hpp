@@ -2,22 +2,23 @@
 //
 // Pipeline of one generation (Algorithm 1 after the first iteration; the
 // first iteration runs the same kernels with the random-init genotype):
-//   k_vary_eval     one wave64 per offspring: draw two parents uniformly from
-//                   the filled cells (Appendix A.2), Iso+LineDD (Algorithm 2)
-//                   gene by gene on coalesced float4 rows of both parents, and
-//                   the objective/descriptor reduction (Appendix B.2) in the
-//                   same pass.  Offspring genotypes are not stored.
-//   k_cell_insert   one thread per offspring: descriptor -> cell (grid bin or
-//                   exact nearest CVT centroid through a bucket grid), then a
-//                   wave-aggregated 64-bit atomicMax of the packed key
-//                   (objective order bits, N_B-1-j) into the cell.
-//   k_regen         one wave per cell: a cell whose key now names an
-//                   offspring regenerates that offspring's genotype into the
-//                   cell's *other* genotype bank (parents stay readable in the
-//                   current bank, so no copy of the batch is ever made).
-//   k_finalize      one workgroup: flip the bank of every new elite, turn its
-//                   key into the incumbent form, and compact the filled cells
-//                   into the ascending list the next selection draws from.
+//   k_vary_eval   one wave64 per offspring: draw two parents uniformly from the
+//                 filled cells (Appendix A.2), Iso+LineDD (Algorithm 2) gene by
+//                 gene on coalesced float4 rows of both parents, the objective /
+//                 descriptor reduction (Appendix B.2).  Offspring genotypes are
+//                 not stored.  (Policies: k_rollout, same outputs.)
+//   k_insert      one thread per offspring: cell (grid bin, or exact nearest
+//                 CVT centroid through a bucket grid) and packed key; keys folded
+//                 per wave and per workgroup (LDS hash), at most one 64-bit
+//                 atomicMax per distinct cell per workgroup.
+//   k_regen       one wave per few cells: a cell whose key now names an
+//                 offspring regenerates that offspring's genotype into the
+//                 cell's other genotype bank (the parents' banks were recorded
+//                 per offspring, so they stay readable), records objective and
+//                 descriptor, then flips its bank and marks the key incumbent.
+//                 One more workgroup of this kernel compacts the filled cells
+//                 (only when a new cell was filled) into the ascending list the
+//                 next selection draws from.
 #pragma once
 
 #include "qd_device.hpp"
@@ -35,6 +36,7 @@ struct Params {
   int obs, hid, act, T;
   Key key;
   int bucket_res, num_buckets;
+  double inv_bucket_res;          // 1 / bucket_res
   uint64_t* arch_key;
   float* arch_fit;
   float* arch_desc;
@@ -46,12 +48,14 @@ struct Params {
   int* bucket_idx;                // [C]
   float* env;
   int* occ_list;
-  int* counters;                  // [0] filled cells, [1] flags
+  int* counters;                  // [0] filled cells, [1] flags, [3] occupancy changed
   int* off_par;
   float* off_fit;
   float* off_desc;
   int* off_cell;
   uint8_t* off_won;
+  uint64_t* off_key;
+  uint8_t* off_bank;              // bank of parent 1 | bank of parent 2 << 1
   float* off_geno;                // [N_B][stride] or null
   double* stats;
 };
@@ -70,6 +74,7 @@ struct Pair {
   const float* row2;
   float lambda;
   int c1, c2;
+  uint32_t banks;
 };
 
 __device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, int nocc) {
@@ -78,8 +83,24 @@ __device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, 
   q.c1 = pick(p.occ_list, x.x, nocc);
   q.c2 = pick(p.occ_list, x.y, nocc);
   q.lambda = p.line_sigma * gauss2(x.z, x.w).x;
-  q.row1 = geno_row(p, p.arch_slot[q.c1], q.c1);
-  q.row2 = geno_row(p, p.arch_slot[q.c2], q.c2);
+  const uint32_t b1 = p.arch_slot[q.c1], b2 = p.arch_slot[q.c2];
+  q.banks = b1 | (b2 << 1);
+  q.row1 = geno_row(p, b1, q.c1);
+  q.row2 = geno_row(p, b2, q.c2);
+  return q;
+}
+
+// The same pair, rebuilt after the generation from what the offspring
+// recorded (cells and banks) -- independent of the archive's current state.
+__device__ __forceinline__ Pair recorded_pair(const Params& p, uint32_t g, int j) {
+  const uint4 x = philox(0u, (uint32_t)j, g, kTagSelect, p.key);
+  Pair q;
+  q.c1 = p.off_par[2 * j];
+  q.c2 = p.off_par[2 * j + 1];
+  q.banks = p.off_bank[j];
+  q.lambda = p.line_sigma * gauss2(x.z, x.w).x;
+  q.row1 = geno_row(p, q.banks & 1u, q.c1);
+  q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
   return q;
 }
 
@@ -122,6 +143,194 @@ __device__ __forceinline__ float task_term(float x) {
 }
 
 // ---------------------------------------------------------------------------
+// Descriptor -> cell.  Every lane of the calling wave holds the same
+// descriptor and gets the same answer.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int grid_cell(const Params& p, const float* d) {
+  int cell = 0;
+  for (int k = 0; k < p.D; ++k) {
+    if (!(d[k] == d[k])) return -1;
+    const float t = (d[k] - p.lo[k]) / p.span[k];
+    const float fb = __builtin_floorf(t * (float)p.grid[k]);
+    const int b = fb < 0.0f ? 0 : (fb > (float)(p.grid[k] - 1) ? p.grid[k] - 1 : (int)fb);
+    cell = cell * p.grid[k] + b;
+  }
+  return cell;
+}
+
+// Exact nearest centroid of u = (d - lo) / (hi - lo): squared distance as an
+// fma chain over dimensions from 0, ties to the lowest centroid index -- the
+// brute-force argmin -- found by one thread through a bucket grid of
+// bucket_res^D cells over the unit box.  Rings of buckets (Chebyshev distance
+// r from the query's bucket) are visited in order until the best distance is
+// certainly below the distance to every unvisited bucket (a relative margin of
+// 1e-5, far above the fp32 rounding of either side).
+template <int D>
+__device__ __forceinline__ void visit_range(const Params& p, int s0, int s1, const float* u,
+                                            float& best, int& best_idx) {
+  for (int s = s0; s < s1; ++s) {
+    const float4 c = p.bucket_pts[s];
+    const float cc[4] = {c.x, c.y, c.z, c.w};
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      const float diff = u[k] - cc[k];
+      acc = fma32(diff, diff, acc);
+    }
+    const int idx = p.bucket_idx[s];
+    if (acc < best || (acc == best && idx < best_idx)) {
+      best = acc;
+      best_idx = idx;
+    }
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void visit_bucket(const Params& p, int bucket, const float* u,
+                                             float& best, int& best_idx) {
+  visit_range<D>(p, p.bucket_start[bucket], p.bucket_start[bucket + 1], u, best, best_idx);
+}
+
+template <int D>
+__device__ int cvt_cell(const Params& p, const float* d) {
+  const int R = p.bucket_res;
+  float u[D];
+  int qb[D];
+#pragma unroll
+  for (int k = 0; k < D; ++k) {
+    if (!(d[k] == d[k])) return -1;
+    u[k] = (d[k] - p.lo[k]) / p.span[k];
+    float fb = __builtin_floorf(u[k] * (float)R);
+    fb = fb < 0.0f ? 0.0f : (fb > (float)(R - 1) ? (float)(R - 1) : fb);
+    qb[k] = (int)fb;
+  }
+  float best = __builtin_inff();
+  int best_idx = 0x7fffffff;
+  int r0 = 0;
+  if (D == 2) {
+    // rings 0 and 1 together: all 9 bucket ranges, then the first centroid of
+    // each bucket, are fetched with independent loads (one round trip each)
+    int st[9], en[9];
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {
+      const int b0 = qb[0] + i / 3 - 1, b1 = qb[1] + i % 3 - 1;
+      const bool in = b0 >= 0 && b0 < R && b1 >= 0 && b1 < R;
+      const int bucket = in ? b0 * R + b1 : 0;
+      st[i] = in ? p.bucket_start[bucket] : 0;
+      en[i] = in ? p.bucket_start[bucket + 1] : 0;
+    }
+    float4 first[9];
+    int fidx[9];
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {
+      const bool any = st[i] < en[i];
+      first[i] = any ? p.bucket_pts[st[i]] : make_float4(0.f, 0.f, 0.f, 0.f);
+      fidx[i] = any ? p.bucket_idx[st[i]] : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {
+      if (st[i] < en[i]) {
+        const float d0 = u[0] - first[i].x;
+        float acc = fma32(d0, d0, 0.0f);
+        const float d1 = u[1] - first[i].y;
+        acc = fma32(d1, d1, acc);
+        if (acc < best || (acc == best && fidx[i] < best_idx)) {
+          best = acc;
+          best_idx = fidx[i];
+        }
+      }
+    }
+    for (int i = 0; i < 9; ++i)
+      if (st[i] + 1 < en[i]) visit_range<D>(p, st[i] + 1, en[i], u, best, best_idx);
+    r0 = 1;
+  }
+  for (int r = r0; r < R; ++r) {
+    if (r > r0 || D != 2) {
+      // the buckets at Chebyshev distance exactly r that lie in the grid
+      if (D == 2) {
+      for (int o0 = -r; o0 <= r; ++o0) {
+        const int b0 = qb[0] + o0;
+        if (b0 < 0 || b0 >= R) continue;
+        const int step = (o0 == -r || o0 == r) ? 1 : 2 * r;
+        for (int o1 = -r; o1 <= r; o1 += step) {
+          const int b1 = qb[1] + o1;
+          if (b1 >= 0 && b1 < R) visit_bucket<D>(p, b0 * R + b1, u, best, best_idx);
+        }
+      }
+    } else {
+      for (int o0 = -r; o0 <= r; ++o0) {
+        const int b0 = qb[0] + o0;
+        if (b0 < 0 || b0 >= R) continue;
+        for (int o1 = -r; o1 <= r; ++o1) {
+          const int b1 = qb[1] + o1;
+          if (b1 < 0 || b1 >= R) continue;
+          for (int o2 = -r; o2 <= r; ++o2) {
+            const int b2 = qb[2] + o2;
+            if (b2 < 0 || b2 >= R) continue;
+            const bool edge = o0 == -r || o0 == r || o1 == -r || o1 == r || o2 == -r || o2 == r;
+            const int step = (edge || r == 0) ? 1 : 2 * r;
+            for (int o3 = -r; o3 <= r; o3 += step) {
+              const int b3 = qb[3] + o3;
+              if (b3 >= 0 && b3 < R)
+                visit_bucket<D>(p, ((b0 * R + b1) * R + b2) * R + b3, u, best, best_idx);
+            }
+          }
+        }
+      }
+    }
+    }
+    // lower bound on the distance to anything outside the visited box
+    double bound = __builtin_inf();
+    bool face = false;
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      if (qb[k] - r >= 1) {
+        const double gap = (double)u[k] - (double)(qb[k] - r) * p.inv_bucket_res - 1e-6;
+        bound = fmin(bound, gap > 0.0 ? gap * gap : 0.0);
+        face = true;
+      }
+      if (qb[k] + r + 1 <= R - 1) {
+        const double gap = (double)(qb[k] + r + 1) * p.inv_bucket_res - (double)u[k] - 1e-6;
+        bound = fmin(bound, gap > 0.0 ? gap * gap : 0.0);
+        face = true;
+      }
+    }
+    if (!face) break;
+    if (best_idx != 0x7fffffff && (double)best * (1.0 + 1e-5) < bound) break;
+  }
+  return best_idx;
+}
+
+// Insertion key: order-preserving bits of the objective (-0 as +0), then
+// N_B-1-j so that equal objectives go to the lowest batch index; 0 = none.
+__device__ __forceinline__ uint64_t insert_key(const Params& p, float f, int cell, int j) {
+  return cell < 0 ? 0ull
+                  : ((uint64_t)order_bits(f) << 32) | (uint64_t)(uint32_t)(p.nb - 1 - j);
+}
+
+// Writes the batch outputs of offspring j (called by one lane).
+__device__ __forceinline__ void record_offspring(const Params& p, int j, const Pair& q, float f,
+                                                 const float* d) {
+  p.off_fit[j] = f;
+  for (int k = 0; k < p.D; ++k) p.off_desc[(size_t)j * p.D + k] = d[k];
+  p.off_par[2 * j] = q.c1;
+  p.off_par[2 * j + 1] = q.c2;
+  p.off_bank[j] = (uint8_t)q.banks;
+  p.off_won[j] = 0;
+}
+
+__device__ __forceinline__ void record_empty_archive(const Params& p, int j) {
+  p.off_fit[j] = __builtin_nanf("");
+  p.off_par[2 * j] = -1;
+  p.off_par[2 * j + 1] = -1;
+  p.off_bank[j] = 0;
+  p.off_cell[j] = -1;
+  p.off_key[j] = 0ull;
+  p.off_won[j] = 0;
+  atomicOr(reinterpret_cast<unsigned int*>(p.counters + 1), 1u);
+}
+
+// ---------------------------------------------------------------------------
 // Select + vary + evaluate, one wave per offspring (test functions).
 // Lane l owns genes 256c + 4l .. 256c + 4l + 3 of every chunk c, i.e. gene
 // groups q = g/4 with q mod 64 = l; its partial sums run in ascending gene
@@ -133,17 +342,11 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (j >= p.nb) return;
 
-  Pair q{nullptr, nullptr, 0.0f, -1, -1};
+  Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
   if (!GEN0) {
     const int nocc = p.counters[0];
     if (nocc <= 0) {
-      if (lane == 0) {
-        p.off_fit[j] = __builtin_nanf("");
-        p.off_par[2 * j] = -1;
-        p.off_par[2 * j + 1] = -1;
-        p.off_won[j] = 0;
-        atomicOr(reinterpret_cast<unsigned int*>(p.counters + 1), 1u);
-      }
+      if (lane == 0) record_empty_archive(p, j);
       return;
     }
     q = select_pair(p, g, j, nocc);
@@ -204,145 +407,31 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
     }
   }
   const float total = wave_fold_sum(acc);
-  float d0, d1;
+  float d[2];
   if (TASK == kTaskProj) {
-    d0 = wave_fold_sum(dlo) / (float)half;
-    d1 = wave_fold_sum(dhi) / (float)(n - half);
+    d[0] = wave_fold_sum(dlo) / (float)half;
+    d[1] = wave_fold_sum(dhi) / (float)(n - half);
   } else {
-    d0 = clip(g0, p.lo[0], p.hi[0]);
-    d1 = clip(g1, p.lo[1], p.hi[1]);
+    d[0] = clip(g0, p.lo[0], p.hi[0]);
+    d[1] = clip(g1, p.lo[1], p.hi[1]);
   }
-  if (lane == 0) {
-    p.off_fit[j] = -total;
-    p.off_desc[2 * j] = d0;
-    p.off_desc[2 * j + 1] = d1;
-    p.off_par[2 * j] = q.c1;
-    p.off_par[2 * j + 1] = q.c2;
-    p.off_won[j] = 0;
-  }
+  if (lane == 0) record_offspring(p, j, q, -total, d);
 }
 
 // ---------------------------------------------------------------------------
-// Descriptor -> cell.
+// Insertion.  One thread per offspring finds its cell and packs its key; keys
+// are then folded per wave (lanes sharing a cell) and per workgroup in an LDS
+// hash table, so each workgroup issues at most one global 64-bit atomicMax per
+// distinct cell it saw -- and none when a plain read of the cell's key already
+// shows a key at least as large (keys only grow, so a stale read can only make
+// the workgroup do an atomic it did not need).  A batch crowding into a few
+// cells therefore does not serialise on them.  An atomic that finds an empty
+// cell raises the "occupancy changed" flag read by the compaction.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int grid_cell(const Params& p, const float* d) {
-  int cell = 0;
-  for (int k = 0; k < p.D; ++k) {
-    if (!(d[k] == d[k])) return -1;
-    const float t = (d[k] - p.lo[k]) / p.span[k];
-    const float fb = __builtin_floorf(t * (float)p.grid[k]);
-    const int b = fb < 0.0f ? 0 : (fb > (float)(p.grid[k] - 1) ? p.grid[k] - 1 : (int)fb);
-    cell = cell * p.grid[k] + b;
-  }
-  return cell;
-}
-
-// Exact nearest centroid (squared distance as an fma chain over dimensions,
-// ties to the lowest index) through a bucket grid of bucket_res^D cells over
-// the unit box.  Rings of buckets around the query's bucket are visited in
-// Chebyshev order until the best distance found is certainly below the
-// distance to every unvisited bucket (with a relative margin far above the
-// fp32 rounding of either side), so the answer equals the brute-force argmin.
-template <int D>
-__device__ __forceinline__ void visit_bucket(const Params& p, int bucket, const float* u,
-                                             float& best, int& best_idx) {
-  const int s0 = p.bucket_start[bucket], s1 = p.bucket_start[bucket + 1];
-  for (int s = s0; s < s1; ++s) {
-    const float4 c = p.bucket_pts[s];
-    const float cc[4] = {c.x, c.y, c.z, c.w};
-    float acc = 0.0f;
-#pragma unroll
-    for (int k = 0; k < D; ++k) {
-      const float diff = u[k] - cc[k];
-      acc = fma32(diff, diff, acc);
-    }
-    const int idx = p.bucket_idx[s];
-    if (acc < best || (acc == best && idx < best_idx)) {
-      best = acc;
-      best_idx = idx;
-    }
-  }
-}
-
-template <int D>
-__device__ int cvt_cell(const Params& p, const float* d) {
-  const int R = p.bucket_res;
-  float u[D];
-  int qb[D];
-#pragma unroll
-  for (int k = 0; k < D; ++k) {
-    if (!(d[k] == d[k])) return -1;
-    u[k] = (d[k] - p.lo[k]) / p.span[k];
-    float fb = __builtin_floorf(u[k] * (float)R);
-    fb = fb < 0.0f ? 0.0f : (fb > (float)(R - 1) ? (float)(R - 1) : fb);
-    qb[k] = (int)fb;
-  }
-  float best = __builtin_inff();
-  int best_idx = 0x7fffffff;
-  const double invR = 1.0 / (double)R;
-  for (int r = 0; r < R; ++r) {
-    // buckets at Chebyshev distance exactly r, in range
-    if (D == 2) {
-      for (int o0 = -r; o0 <= r; ++o0) {
-        const int b0 = qb[0] + o0;
-        if (b0 < 0 || b0 >= R) continue;
-        const int step = (o0 == -r || o0 == r) ? 1 : 2 * r;
-        for (int o1 = -r; o1 <= r; o1 += step) {
-          const int b1 = qb[1] + o1;
-          if (b1 >= 0 && b1 < R) visit_bucket<D>(p, b0 * R + b1, u, best, best_idx);
-        }
-      }
-    } else {
-      for (int o0 = -r; o0 <= r; ++o0) {
-        const int b0 = qb[0] + o0;
-        if (b0 < 0 || b0 >= R) continue;
-        for (int o1 = -r; o1 <= r; ++o1) {
-          const int b1 = qb[1] + o1;
-          if (b1 < 0 || b1 >= R) continue;
-          for (int o2 = -r; o2 <= r; ++o2) {
-            const int b2 = qb[2] + o2;
-            if (b2 < 0 || b2 >= R) continue;
-            const bool edge = o0 == -r || o0 == r || o1 == -r || o1 == r || o2 == -r || o2 == r;
-            const int step = edge ? 1 : (r == 0 ? 1 : 2 * r);
-            for (int o3 = -r; o3 <= r; o3 += step) {
-              const int b3 = qb[3] + o3;
-              if (b3 >= 0 && b3 < R)
-                visit_bucket<D>(p, ((b0 * R + b1) * R + b2) * R + b3, u, best, best_idx);
-            }
-          }
-        }
-      }
-    }
-    // lower bound on the distance to anything outside the visited box
-    double bound = __builtin_inf();
-    bool face = false;
-#pragma unroll
-    for (int k = 0; k < D; ++k) {
-      if (qb[k] - r >= 1) {
-        const double gap = (double)u[k] - (double)(qb[k] - r) * invR - 1e-6;
-        bound = fmin(bound, gap > 0.0 ? gap * gap : 0.0);
-        face = true;
-      }
-      if (qb[k] + r + 1 <= R - 1) {
-        const double gap = (double)(qb[k] + r + 1) * invR - (double)u[k] - 1e-6;
-        bound = fmin(bound, gap > 0.0 ? gap * gap : 0.0);
-        face = true;
-      }
-    }
-    if (!face) break;
-    if (best_idx != 0x7fffffff && (double)best * (1.0 + 1e-5) < bound) break;
-  }
-  return best_idx;
-}
-
-// Cell of each offspring, then insertion by packed-key maximum.  Keys are
-// folded per wave (lanes sharing a cell), then per workgroup in an LDS hash
-// table, so each workgroup issues one global 64-bit atomicMax per distinct
-// cell it saw -- a batch crowding into a few cells does not serialise on them.
 constexpr int kInsertBlock = 256, kInsertSlots = 512;
 
 template <int TESS, int D>
-__global__ __launch_bounds__(kInsertBlock) void k_cell_insert(const Params p) {
+__global__ __launch_bounds__(kInsertBlock) void k_insert(const Params p) {
   __shared__ int tag[kInsertSlots];
   __shared__ unsigned long long kmax[kInsertSlots];
   for (int e = threadIdx.x; e < kInsertSlots; e += kInsertBlock) {
@@ -352,7 +441,7 @@ __global__ __launch_bounds__(kInsertBlock) void k_cell_insert(const Params p) {
   __syncthreads();
   const int j = blockIdx.x * kInsertBlock + threadIdx.x;
   int cell = -1;
-  uint64_t key = 0;
+  uint64_t key = 0ull;
   if (j < p.nb) {
     const float f = p.off_fit[j];
     if (f == f) {
@@ -361,9 +450,9 @@ __global__ __launch_bounds__(kInsertBlock) void k_cell_insert(const Params p) {
       for (int k = 0; k < D; ++k) d[k] = p.off_desc[(size_t)j * D + k];
       cell = TESS == kTessGrid ? grid_cell(p, d) : cvt_cell<D>(p, d);
     }
+    key = insert_key(p, f, cell, j);
     p.off_cell[j] = cell;
-    if (cell >= 0)
-      key = ((uint64_t)order_bits(f) << 32) | (uint64_t)(uint32_t)(p.nb - 1 - j);
+    p.off_key[j] = key;
   }
   uint64_t todo = __ballot(cell >= 0);
   while (todo) {
@@ -392,67 +481,39 @@ __global__ __launch_bounds__(kInsertBlock) void k_cell_insert(const Params p) {
   __syncthreads();
   for (int e = threadIdx.x; e < kInsertSlots; e += kInsertBlock) {
     const int c = tag[e];
-    if (c >= 0) atomicMax((unsigned long long*)&p.arch_key[c], kmax[e]);
+    if (c < 0) continue;
+    const unsigned long long k = kmax[e];
+    unsigned long long* slot = (unsigned long long*)&p.arch_key[c];
+    if (k <= *slot) continue;
+    if (atomicMax(slot, k) == 0ull) p.counters[3] = 1;
   }
 }
 
 // ---------------------------------------------------------------------------
-// Winners: one wave per cell regenerates the winning offspring's genotype into
-// the cell's other bank and records its objective and descriptor.
+// Compaction of the filled cells into the ascending list the next selection
+// draws from (Appendix A.2).  Run by one extra workgroup of the winner kernel,
+// only when an insertion filled a new cell (counters[3]); it clears that flag.
+// The winner workgroups running beside it change keys only from one non-zero
+// value to another, so filled/empty is already final.
 // ---------------------------------------------------------------------------
-constexpr int kRegenCellsPerWave = 8;
+constexpr int kCompactItems = 16;
 
-template <bool GEN0>
-__global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
-  const int lane = threadIdx.x & 63;
-  const int first = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kRegenCellsPerWave;
-  for (int c = first; c < first + kRegenCellsPerWave && c < p.C; ++c) {
-    const uint64_t key = p.arch_key[c];
-    const uint32_t low = (uint32_t)key;
-    if (key == 0ull || low == 0xffffffffu) continue;
-    const int j = p.nb - 1 - (int)low;
-    Pair q{nullptr, nullptr, 0.0f, -1, -1};
-    if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
-    float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
-    for (int base = 4 * lane; base < p.n; base += 256)
-      *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
-    if (lane == 0) {
-      p.arch_fit[c] = p.off_fit[j];
-      for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
-      p.off_won[j] = 1;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Finalize: new elites switch bank and become incumbents (low word all ones,
-// so a later offspring needs a strictly greater objective); then the filled
-// cells are compacted in ascending order.  One workgroup of 1024 threads.
-// ---------------------------------------------------------------------------
-constexpr int kFinalizeItems = 16;
-
-__global__ __launch_bounds__(1024) void k_finalize(const Params p) {
-  __shared__ int wave_tot[16];
+__device__ void compact_filled(const Params& p) {
+  constexpr int kThreads = 256;
+  __shared__ int wave_tot[kThreads / 64];
   __shared__ int base_sh;
+  if (p.counters[3] == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) base_sh = 0;
-  for (int start = 0; start < p.C; start += 1024 * kFinalizeItems) {
-    // each thread owns kFinalizeItems consecutive cells; all loads first
-    const int c0 = start + tid * kFinalizeItems;
-    uint64_t keys[kFinalizeItems];
+  for (int start = 0; start < p.C; start += kThreads * kCompactItems) {
+    const int c0 = start + tid * kCompactItems;
+    uint64_t keys[kCompactItems];
 #pragma unroll
-    for (int i = 0; i < kFinalizeItems; ++i) keys[i] = c0 + i < p.C ? p.arch_key[c0 + i] : 0ull;
-    int cnt = 0;
+    for (int i = 0; i < kCompactItems; ++i) keys[i] = c0 + i < p.C ? p.arch_key[c0 + i] : 0ull;
+    uint32_t filled = 0u;
 #pragma unroll
-    for (int i = 0; i < kFinalizeItems; ++i) {
-      if (keys[i] != 0ull) {
-        ++cnt;
-        if ((uint32_t)keys[i] != 0xffffffffu) {
-          p.arch_slot[c0 + i] ^= 1u;
-          p.arch_key[c0 + i] = keys[i] | 0xffffffffull;
-        }
-      }
-    }
+    for (int i = 0; i < kCompactItems; ++i) filled |= (keys[i] != 0ull ? 1u : 0u) << i;
+    const int cnt = __popc(filled);
     int incl = cnt;
 #pragma unroll
     for (int h = 1; h < 64; h <<= 1) {
@@ -464,17 +525,73 @@ __global__ __launch_bounds__(1024) void k_finalize(const Params p) {
     int off = base_sh + incl - cnt;
     for (int w = 0; w < wave; ++w) off += wave_tot[w];
 #pragma unroll
-    for (int i = 0; i < kFinalizeItems; ++i)
-      if (keys[i] != 0ull) p.occ_list[off++] = c0 + i;
+    for (int i = 0; i < kCompactItems; ++i)
+      if ((filled >> i) & 1u) p.occ_list[off++] = c0 + i;
     __syncthreads();
     if (tid == 0) {
       int tot = 0;
-      for (int w = 0; w < 16; ++w) tot += wave_tot[w];
+      for (int w = 0; w < kThreads / 64; ++w) tot += wave_tot[w];
       base_sh += tot;
     }
     __syncthreads();
   }
-  if (tid == 0) p.counters[0] = base_sh;
+  if (tid == 0) {
+    p.counters[0] = base_sh;
+    p.counters[3] = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Winners: a workgroup takes kRegenCells consecutive cells.  For each cell
+// whose key names an offspring, its four waves regenerate that offspring's
+// genotype (256-gene chunks shared out over the waves) into the cell's other
+// bank from the recorded parents.  After a barrier the cells record objective
+// and descriptor, switch to the new bank, and turn the key into the incumbent
+// form (low word all ones: a later offspring must be strictly better).
+// ---------------------------------------------------------------------------
+constexpr int kRegenCells = 8;
+
+__device__ __forceinline__ void finish_winner(const Params& p, int c, int j, uint64_t key) {
+  p.arch_fit[c] = p.off_fit[j];
+  for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
+  p.off_won[j] = 1;
+  p.arch_slot[c] ^= 1u;
+  p.arch_key[c] = key | 0xffffffffull;
+}
+
+__device__ __forceinline__ bool names_offspring(uint64_t key) {
+  return key != 0ull && (uint32_t)key != 0xffffffffu;
+}
+
+// Workgroups 0 .. ceil(C / kRegenCells) - 1 take cells; one more compacts.
+inline unsigned regen_blocks(int C) { return (unsigned)((C + kRegenCells - 1) / kRegenCells) + 1u; }
+
+template <bool GEN0>
+__global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
+  if (blockIdx.x == gridDim.x - 1) {
+    compact_filled(p);
+    return;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int first = blockIdx.x * kRegenCells;
+  for (int c = first; c < first + kRegenCells && c < p.C; ++c) {
+    const uint64_t key = p.arch_key[c];
+    if (!names_offspring(key)) continue;
+    const int j = p.nb - 1 - (int)(uint32_t)key;
+    Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
+    if (!GEN0) q = recorded_pair(p, g, j);
+    float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
+    for (int base = 256 * wave + 4 * lane; base < p.n; base += 1024)
+      *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
+  }
+  __syncthreads();
+  if (threadIdx.x < kRegenCells) {
+    const int c = first + threadIdx.x;
+    if (c < p.C) {
+      const uint64_t key = p.arch_key[c];
+      if (names_offspring(key)) finish_winner(p, c, p.nb - 1 - (int)(uint32_t)key, key);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------

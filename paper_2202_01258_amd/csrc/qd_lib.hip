@@ -116,6 +116,8 @@ qd_status make_layout(const qd_config* c, qd_layout* L) {
   bytes[QD_BUF_OFF_DESC] = 4 * nb * D;
   bytes[QD_BUF_OFF_CELL] = 4 * nb;
   bytes[QD_BUF_OFF_WON] = nb;
+  bytes[QD_BUF_OFF_KEY] = 8 * nb;
+  bytes[QD_BUF_OFF_BANK] = nb;
   bytes[QD_BUF_OFF_GENO] = c->keep_offspring ? 4 * nb * stride : 0;
   bytes[QD_BUF_STATS] = 8 * 8;
   uint64_t off = 0;
@@ -209,16 +211,16 @@ void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
 #undef QD_VE
 }
 
-void launch_cell_insert(qd_archive* h, hipStream_t s) {
+void launch_insert(qd_archive* h, hipStream_t s) {
   const qd::Params& p = h->p;
-  Timed t(h, s, QD_K_CELL_INSERT);
+  Timed t(h, s, QD_K_INSERT);
   const dim3 grid(blocks_for((uint64_t)p.nb, qd::kInsertBlock)), block(qd::kInsertBlock);
   if (p.tess == qd::kTessGrid) {
-    if (p.D == 2) hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessGrid, 2>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessGrid, 4>), grid, block, 0, s, p);
+    if (p.D == 2) hipLaunchKernelGGL((qd::k_insert<qd::kTessGrid, 2>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((qd::k_insert<qd::kTessGrid, 4>), grid, block, 0, s, p);
   } else {
-    if (p.D == 2) hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessCvt, 2>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((qd::k_cell_insert<qd::kTessCvt, 4>), grid, block, 0, s, p);
+    if (p.D == 2) hipLaunchKernelGGL((qd::k_insert<qd::kTessCvt, 2>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((qd::k_insert<qd::kTessCvt, 4>), grid, block, 0, s, p);
   }
 }
 
@@ -226,14 +228,9 @@ template <bool GEN0>
 void launch_regen(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
   Timed t(h, s, QD_K_REGEN);
-  const dim3 grid(blocks_for((uint64_t)p.C, 4 * qd::kRegenCellsPerWave)), block(256);
+  const dim3 grid(qd::regen_blocks(p.C)), block(256);
   if (p.task == qd::kTaskMlp) qd::launch_mlp_regen(p, GEN0, g, s);
   else hipLaunchKernelGGL((qd::k_regen<GEN0>), grid, block, 0, s, p, g);
-}
-
-void launch_finalize(qd_archive* h, hipStream_t s) {
-  Timed t(h, s, QD_K_FINALIZE);
-  hipLaunchKernelGGL(qd::k_finalize, dim3(1), dim3(1024), 0, s, h->p);
 }
 
 template <bool GEN0>
@@ -244,9 +241,8 @@ qd_status enqueue_generation(qd_archive* h, hipStream_t s, uint32_t g) {
   } else {
     launch_vary_eval<GEN0>(h, s, g);
   }
-  launch_cell_insert(h, s);
+  launch_insert(h, s);
   launch_regen<GEN0>(h, s, g);
-  launch_finalize(h, s);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? QD_OK : hip_fail(e);
 }
@@ -282,6 +278,7 @@ qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
   p.key.k0 = (uint32_t)(c->seed & 0xffffffffull);
   p.key.k1 = (uint32_t)(c->seed >> 32);
   p.bucket_res = L->bucket_res;
+  p.inv_bucket_res = L->bucket_res > 0 ? 1.0 / (double)L->bucket_res : 0.0;
   p.num_buckets = L->num_buckets;
   auto at = [&](int b) -> void* { return L->bytes[b] ? ws + L->offset[b] : nullptr; };
   p.arch_key = (uint64_t*)at(QD_BUF_ARCHIVE_KEY);
@@ -303,6 +300,8 @@ qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
   p.off_desc = (float*)at(QD_BUF_OFF_DESC);
   p.off_cell = (int*)at(QD_BUF_OFF_CELL);
   p.off_won = (uint8_t*)at(QD_BUF_OFF_WON);
+  p.off_key = (uint64_t*)at(QD_BUF_OFF_KEY);
+  p.off_bank = (uint8_t*)at(QD_BUF_OFF_BANK);
   p.off_geno = (float*)at(QD_BUF_OFF_GENO);
   p.stats = (double*)at(QD_BUF_STATS);
   return p;

@@ -101,17 +101,11 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   const int o = threadIdx.x;
   const int j = blockIdx.x;
 
-  Pair q{nullptr, nullptr, 0.0f, -1, -1};
+  Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
   if (!GEN0) {
     const int nocc = p.counters[0];
     if (nocc <= 0) {
-      if (o == 0) {
-        p.off_fit[j] = __builtin_nanf("");
-        p.off_par[2 * j] = -1;
-        p.off_par[2 * j + 1] = -1;
-        p.off_won[j] = 0;
-        atomicOr(reinterpret_cast<unsigned int*>(p.counters + 1), 1u);
-      }
+      if (o == 0) record_empty_archive(p, j);
       return;
     }
     q = select_pair(p, g, j, nocc);
@@ -209,6 +203,7 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     p.off_fit[j] = ret;
     p.off_par[2 * j] = q.c1;
     p.off_par[2 * j + 1] = q.c2;
+    p.off_bank[j] = (uint8_t)q.banks;
     p.off_won[j] = 0;
   } else if (o <= 4) {
     p.off_desc[(size_t)j * 4 + (o - 1)] = dsum / (float)p.T;
@@ -219,23 +214,29 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
 // genotype into the cell's other bank (same gene formula as the prologue).
 template <bool GEN0>
 __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
-  const int lane = threadIdx.x & 63;
-  const int first = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kRegenCellsPerWave;
-  for (int c = first; c < first + kRegenCellsPerWave && c < p.C; ++c) {
+  if (blockIdx.x == gridDim.x - 1) {
+    compact_filled(p);
+    return;
+  }
+  const int tid = threadIdx.x;
+  const int first = blockIdx.x * kRegenCells;
+  const int nblk = (p.n + 3) >> 2;
+  for (int c = first; c < first + kRegenCells && c < p.C; ++c) {
     const uint64_t key = p.arch_key[c];
-    const uint32_t low = (uint32_t)key;
-    if (key == 0ull || low == 0xffffffffu) continue;
-    const int j = p.nb - 1 - (int)low;
-    Pair q{nullptr, nullptr, 0.0f, -1, -1};
-    if (!GEN0) q = select_pair(p, g, j, p.counters[0]);
+    if (!names_offspring(key)) continue;
+    const int j = p.nb - 1 - (int)(uint32_t)key;
+    Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
+    if (!GEN0) q = recorded_pair(p, g, j);
     float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
-    const int nblk = (p.n + 3) >> 2;
-    for (int blk = lane; blk < nblk; blk += 64)
+    for (int blk = tid; blk < nblk; blk += 256)
       *reinterpret_cast<float4*>(dst + 4 * blk) = mlp_gene_block<GEN0>(p, q, g, j, blk);
-    if (lane == 0) {
-      p.arch_fit[c] = p.off_fit[j];
-      for (int k = 0; k < p.D; ++k) p.arch_desc[(size_t)c * p.D + k] = p.off_desc[(size_t)j * p.D + k];
-      p.off_won[j] = 1;
+  }
+  __syncthreads();
+  if (tid < kRegenCells) {
+    const int c = first + tid;
+    if (c < p.C) {
+      const uint64_t key = p.arch_key[c];
+      if (names_offspring(key)) finish_winner(p, c, p.nb - 1 - (int)(uint32_t)key, key);
     }
   }
 }
@@ -258,8 +259,7 @@ inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hi
 }
 
 inline void launch_mlp_regen(const Params& p, bool gen0, uint32_t g, hipStream_t s) {
-  const dim3 grid((unsigned)((p.C + 4 * kRegenCellsPerWave - 1) / (4 * kRegenCellsPerWave))),
-      block(256);
+  const dim3 grid(regen_blocks(p.C)), block(256);
   if (gen0) hipLaunchKernelGGL((k_regen_mlp<true>), grid, block, 0, s, p, g);
   else hipLaunchKernelGGL((k_regen_mlp<false>), grid, block, 0, s, p, g);
 }

@@ -21,11 +21,11 @@ QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
 
 (BUF_ARCHIVE_KEY, BUF_ARCHIVE_FIT, BUF_ARCHIVE_DESC, BUF_ARCHIVE_SLOT, BUF_ARCHIVE_GENO,
  BUF_CENTROIDS, BUF_BUCKET_START, BUF_BUCKET_ITEMS, BUF_ENV, BUF_OCC_LIST, BUF_COUNTERS,
- BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC, BUF_OFF_CELL, BUF_OFF_WON, BUF_OFF_GENO,
- BUF_STATS, NUM_BUFFERS) = range(19)
+ BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC, BUF_OFF_CELL, BUF_OFF_WON, BUF_OFF_KEY,
+ BUF_OFF_BANK, BUF_OFF_GENO, BUF_STATS, NUM_BUFFERS) = range(21)
 
-(K_VARY_EVAL, K_ROLLOUT, K_CELL_INSERT, K_REGEN, K_FINALIZE, K_SETUP, NUM_KERNELS) = range(7)
-KERNEL_NAMES = ["vary_eval", "rollout", "cell_insert", "regen", "finalize", "setup"]
+(K_VARY_EVAL, K_ROLLOUT, K_INSERT, K_REGEN, K_SETUP, NUM_KERNELS) = range(6)
+KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
 
 # Every symbol include/qd.h declares.
 EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_archive_stats",
@@ -240,6 +240,8 @@ class Archive:
             off_desc=self.view(BUF_OFF_DESC, torch.float32, (nb, D)),
             off_cell=self.view(BUF_OFF_CELL, torch.int32, (nb,)),
             off_won=self.view(BUF_OFF_WON, torch.uint8, (nb,)),
+            off_key=self.view(BUF_OFF_KEY, torch.int64, (nb,)),
+            off_bank=self.view(BUF_OFF_BANK, torch.uint8, (nb,)),
             off_geno=self.view(BUF_OFF_GENO, torch.float32, (nb, st)),
         )
 
