@@ -82,25 +82,27 @@ __device__ __forceinline__ float div_narrow(float a, float b) {
 // Square root of a positive normal x (or +-0) without the small-input
 // scaling: hardware estimate, then the neighbour one unit in the last place
 // below or above is taken when the fma residual says the estimate rounded
-// the wrong way.  Checked against IEEE sqrt like div_narrow.
+// the wrong way.  (For x = +-0 both neighbours fail their test, so +-0 comes
+// back unchanged.)  Checked against IEEE sqrt like div_narrow.
 __device__ __forceinline__ float sqrt_normal(float x) {
   const float s = __builtin_amdgcn_sqrtf(x);
   const float dn = __uint_as_float(__float_as_uint(s) - 1u);
   const float up = __uint_as_float(__float_as_uint(s) + 1u);
-  float r = fma32(-dn, s, x) <= 0.0f ? dn : s;
-  r = fma32(-up, s, x) > 0.0f ? up : r;
-  return x == 0.0f ? x : r;
+  const float r = fma32(-dn, s, x) <= 0.0f ? dn : s;
+  return fma32(-up, s, x) > 0.0f ? up : r;
 }
 
-// ln x for positive normal x.  x = 2^e m, m folded into [sqrt(1/2), sqrt(2));
-// ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd series through s^9.
-// FAST selects div_narrow for the quotient; both give the same bits.
+// ln (x 2^-scale) for positive normal x.  x = 2^e m, m folded into
+// [sqrt(1/2), sqrt(2)); ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd
+// series through s^9.  FAST selects div_narrow for the quotient; both give
+// the same bits.  (A power-of-two factor only moves the exponent, so passing
+// it as `scale` gives the bits of log_pos(x * 2^-scale).)
 template <bool FAST = false>
-__device__ __forceinline__ float log_pos(float x) {
+__device__ __forceinline__ float log_pos(float x, int scale = 0) {
   const uint32_t bits = __float_as_uint(x);
   const uint32_t frac = bits & 0x7fffffu;
   const bool fold = frac > 0x3504f3u;
-  const int e = (int)(bits >> 23) - 127 + (fold ? 1 : 0);
+  const int e = (int)(bits >> 23) - (127 + scale) + (fold ? 1 : 0);
   const float m = __uint_as_float((frac | 0x3f800000u) - (fold ? 0x00800000u : 0u));
   const float s = FAST ? div_narrow(m - 1.0f, m + 1.0f) : (m - 1.0f) / (m + 1.0f);
   const float s2 = s * s;
@@ -133,9 +135,11 @@ __device__ __forceinline__ float cos_small(float x) {
 // (halves rounding up) is split off in integers, leaving (pi/2) f with
 // f = m / 2^22 - q, |f| <= 1/2, exactly.
 __device__ __forceinline__ float2 turn_cos_sin(uint32_t m) {
-  const uint32_t q = (m + 0x200000u) >> 22;
-  const float f = (float)((int32_t)m - (int32_t)(q << 22)) * 0x1p-22f;
-  const float x = f * kHalfPi;
+  const uint32_t t = m + 0x200000u;
+  const uint32_t q = t >> 22;
+  // f * pi/2 with f = rem 2^-22: the power-of-two factor is exact, so it is
+  // folded into the constant and the product still rounds once
+  const float x = (float)((int32_t)(t & 0x3fffffu) - 0x200000) * (kHalfPi * 0x1p-22f);
   const float s = sin_small(x), c = cos_small(x);
   // quarter turns q = 0..3 (4 = 0): (c, s), (-s, c), (-c, -s), (s, -c),
   // written as a swap on odd q and sign flips, without branches
@@ -152,7 +156,8 @@ __device__ __forceinline__ float bm_radius_ieee(uint32_t xa) {
   return __builtin_sqrtf(-2.0f * log_pos<false>(unit24_open0(xa)));
 }
 __device__ __forceinline__ float bm_radius(uint32_t xa) {
-  return sqrt_normal(-2.0f * log_pos<true>(unit24_open0(xa)));
+  // unit24_open0(xa) = ((xa >> 8) + 1) 2^-24: the 2^-24 goes to the exponent
+  return sqrt_normal(-2.0f * log_pos<true>((float)((xa >> 8) + 1u), 24));
 }
 
 // Two standard normals (Box-Muller) from two Philox words.
