@@ -165,12 +165,13 @@ qd_status qd_set_kernel_timing(qd_archive* h, uint32_t kernel_mask);
  * them.  ms and counts must hold QD_NUM_KERNELS entries. */
 qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts);
 
-/* Self-check of the short division and square-root sequences the Box-Muller
- * sampler uses in place of IEEE division and square root: for every one of the
- * 2^24 possible radius inputs, compares the two and stores the number of
- * differing results in *mismatches (0 means the sampler's output equals the
- * IEEE-arithmetic definition bit for bit).  d_scratch: 8 bytes of device
- * memory owned by the caller, 8-byte aligned.  Synchronises `stream`. */
+/* Self-check of the short division and square-root sequences the kernels use
+ * in place of IEEE division and square root, over every input each can
+ * receive: mismatches[0] counts the Box-Muller radius inputs (all 2^24) whose
+ * result differs from the IEEE-arithmetic definition, mismatches[1] the fp32
+ * inputs of tanh (all 2^32), mismatches[2] those of sigmoid in [-1, 1]
+ * (zeros mean bit-identical results).  d_scratch: 24 bytes of device memory
+ * owned by the caller, 8-byte aligned.  Synchronises `stream`. */
 qd_status qd_check_fast_arith(void* d_scratch, void* stream, uint64_t* mismatches);
 
 /* Frees the host handle (not the workspace).  NULL is accepted. */

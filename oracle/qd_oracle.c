@@ -313,6 +313,10 @@ int32_t or_cvt_cell(const float* d, int32_t D, const float* lo, const float* hi,
 /* output.  Genotype = [W1 (hid x obs), b1, W2 (hid x hid), b2, W3 (act x    */
 /* hid), b3], row-major.  Return = sum_t (s_{t+1}[0] - 0.5 |a_t|^2);          */
 /* descriptor k = mean over t = 1..T of sigmoid(s_t[k+1]), k = 0..3.          */
+/* Summation order: hidden layers take the bias, then their inputs in order.  */
+/* The output layer sums 8 contiguous slices of hid/8 inputs each, folds the  */
+/* 8 partial sums pairwise (s with s+4, then s+2, then s+1) and adds the bias. */
+/* The dynamics add the two products A s and B a, each summed in order.       */
 /* ------------------------------------------------------------------------ */
 static void dense_tanh(const float* W, const float* bias, const float* in, int32_t nin,
                        int32_t nout, float* out) {
@@ -320,6 +324,23 @@ static void dense_tanh(const float* W, const float* bias, const float* in, int32
     float acc = bias[o];
     for (int32_t k = 0; k < nin; ++k) acc = fmaf(W[(size_t)o * nin + k], in[k], acc);
     out[o] = or_tanhf(acc);
+  }
+}
+
+static void dense_tanh_sliced8(const float* W, const float* bias, const float* in, int32_t nin,
+                               int32_t nout, float* out) {
+  const int32_t len = nin / 8;
+  for (int32_t o = 0; o < nout; ++o) {
+    float part[8];
+    for (int32_t sl = 0; sl < 8; ++sl) {
+      float acc = 0.0f;
+      for (int32_t k = sl * len; k < (sl + 1) * len; ++k)
+        acc = fmaf(W[(size_t)o * nin + k], in[k], acc);
+      part[sl] = acc;
+    }
+    for (int32_t h = 4; h >= 1; h >>= 1)
+      for (int32_t sl = 0; sl < h; ++sl) part[sl] = part[sl] + part[sl + h];
+    out[o] = or_tanhf(part[0] + bias[o]);
   }
 }
 
@@ -343,12 +364,12 @@ void or_mlp_rollout(const float* w, int32_t obs, int32_t hid, int32_t act, int32
   for (int32_t t = 0; t < T; ++t) {
     dense_tanh(W1, b1, s, obs, hid, h1);
     dense_tanh(W2, b2, h1, hid, hid, h2);
-    dense_tanh(W3, b3, h2, hid, act, a);
+    dense_tanh_sliced8(W3, b3, h2, hid, act, a);
     for (int32_t i = 0; i < obs; ++i) {
-      float acc = 0.0f;
-      for (int32_t k = 0; k < obs; ++k) acc = fmaf(A[(size_t)i * obs + k], s[k], acc);
-      for (int32_t k = 0; k < act; ++k) acc = fmaf(B[(size_t)i * act + k], a[k], acc);
-      sn[i] = or_tanhf(acc);
+      float as = 0.0f, ba = 0.0f;
+      for (int32_t k = 0; k < obs; ++k) as = fmaf(A[(size_t)i * obs + k], s[k], as);
+      for (int32_t k = 0; k < act; ++k) ba = fmaf(B[(size_t)i * act + k], a[k], ba);
+      sn[i] = or_tanhf(as + ba);
     }
     float q = 0.0f;
     for (int32_t o = 0; o < act; ++o) q = fmaf(a[o], a[o], q);

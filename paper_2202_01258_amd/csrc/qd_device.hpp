@@ -199,8 +199,20 @@ __device__ __forceinline__ float exp32(float x) {
   return x == x ? e : x;
 }
 
+// a / b by the hardware reciprocal and one residual correction.  Used where
+// the library has checked, over every input the caller can pass, that the
+// result equals the IEEE quotient (qd_check_fast_arith).
+__device__ __forceinline__ float div_rcp(float a, float b) {
+  const float y = __builtin_amdgcn_rcpf(b);
+  const float q = a * y;
+  const float r = fma32(-q, b, a);
+  return fma32(r, y, q);
+}
+
 // tanh: odd Taylor polynomial through x^11 for |x| < 0.3,
-// else 1 - 2 / (e^{2|x|} + 1); the sign is copied back.
+// else 1 - 2 / (e^{2|x|} + 1); the sign is copied back.  FAST takes the
+// quotient from div_rcp (same bits for every fp32 input).
+template <bool FAST = true>
 __device__ __forceinline__ float tanh32(float x) {
   const float a = __builtin_fabsf(x);
   float r;
@@ -212,12 +224,19 @@ __device__ __forceinline__ float tanh32(float x) {
     p = fma32(a2, p, -1.0f / 3.0f);
     r = fma32(a * a2, p, a);
   } else {
-    r = 1.0f - 2.0f / (exp32(a + a) + 1.0f);
+    const float d = exp32(a + a) + 1.0f;
+    r = 1.0f - (FAST ? div_rcp(2.0f, d) : 2.0f / d);
   }
   return __builtin_copysignf(r, x);
 }
 
-__device__ __forceinline__ float sigmoid32(float x) { return 1.0f / (1.0f + exp32(-x)); }
+// 1 / (1 + e^{-x}); FAST as for tanh32 (same bits for |x| <= 1, the range of
+// the tanh states it is applied to).
+template <bool FAST = true>
+__device__ __forceinline__ float sigmoid32(float x) {
+  const float d = 1.0f + exp32(-x);
+  return FAST ? div_rcp(1.0f, d) : 1.0f / d;
+}
 
 // ---------------------------------------------------------------------------
 // Wave64 helpers.

@@ -735,16 +735,34 @@ __global__ void k_env(const Params p, int count) {
     if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
 }
 
-// Self-check of the short division / square-root sequences: the Box-Muller
-// radius for every one of the 2^24 possible 24-bit inputs, against the IEEE
-// operations.  Counts mismatches into *count.
-__global__ void k_zero_u64(unsigned long long* x) { *x = 0ull; }
+// Self-checks of the short division / square-root sequences against the IEEE
+// operations, over every input each one can receive: the Box-Muller radius
+// for all 2^24 inputs, tanh for all 2^32 fp32 bit patterns, sigmoid for all
+// fp32 values in [-1, 1].  Counts results that differ (both NaN = equal).
+__global__ void k_zero_u64(unsigned long long* x) {
+  if (threadIdx.x < 3) x[threadIdx.x] = 0ull;
+}
 
-__global__ __launch_bounds__(256) void k_check_radius(unsigned long long* count) {
-  const uint32_t k = blockIdx.x * 256u + threadIdx.x;       // 0 .. 2^24 - 1
-  const uint32_t xa = k << 8;
-  const float a = bm_radius(xa), b = bm_radius_ieee(xa);
-  if (__float_as_uint(a) != __float_as_uint(b)) atomicAdd(count, 1ull);
+__device__ __forceinline__ bool same_bits(float a, float b) {
+  return __float_as_uint(a) == __float_as_uint(b) || (a != a && b != b);
+}
+
+__global__ __launch_bounds__(256) void k_check_fast(unsigned long long* count) {
+  const uint64_t nthr = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  unsigned long long bad_r = 0, bad_t = 0, bad_s = 0;
+  for (uint64_t k = tid; k < (1ull << 24); k += nthr) {
+    const uint32_t xa = (uint32_t)k << 8;
+    bad_r += same_bits(bm_radius(xa), bm_radius_ieee(xa)) ? 0 : 1;
+  }
+  for (uint64_t k = tid; k < (1ull << 32); k += nthr) {
+    const float x = __uint_as_float((uint32_t)k);
+    bad_t += same_bits(tanh32<true>(x), tanh32<false>(x)) ? 0 : 1;
+    if (__builtin_fabsf(x) <= 1.0f) bad_s += same_bits(sigmoid32<true>(x), sigmoid32<false>(x)) ? 0 : 1;
+  }
+  if (bad_r) atomicAdd(count, bad_r);
+  if (bad_t) atomicAdd(count + 1, bad_t);
+  if (bad_s) atomicAdd(count + 2, bad_s);
 }
 
 }  // namespace qd

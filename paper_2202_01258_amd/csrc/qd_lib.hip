@@ -420,15 +420,15 @@ qd_status qd_check_fast_arith(void* d_scratch, void* stream, uint64_t* mismatche
   if (((uintptr_t)d_scratch % 8) != 0) return QD_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
   auto* count = (unsigned long long*)d_scratch;
-  hipLaunchKernelGGL(qd::k_zero_u64, dim3(1), dim3(1), 0, s, count);
-  hipLaunchKernelGGL(qd::k_check_radius, dim3(1u << 16), dim3(256), 0, s, count);
+  hipLaunchKernelGGL(qd::k_zero_u64, dim3(1), dim3(64), 0, s, count);
+  hipLaunchKernelGGL(qd::k_check_fast, dim3(1u << 15), dim3(256), 0, s, count);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e);
-  unsigned long long host = 0;
-  e = hipMemcpyAsync(&host, count, sizeof(host), hipMemcpyDeviceToHost, s);
+  unsigned long long host[3] = {0, 0, 0};
+  e = hipMemcpyAsync(host, count, sizeof(host), hipMemcpyDeviceToHost, s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) return hip_fail(e);
-  *mismatches = host;
+  for (int k = 0; k < 3; ++k) mismatches[k] = host[k];
   return QD_OK;
 }
 

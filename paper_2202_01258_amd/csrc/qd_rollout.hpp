@@ -6,11 +6,10 @@
 // batch of independent GEMV chains, not one GEMM: no matrix core applies.
 //
 // One workgroup of H threads (H = hidden width, one or two waves) runs one
-// individual.  Thread o keeps row o of W1 and W2 and the biases b1[o], b2[o]
-// in VGPRs for the whole episode; W3 and b3 live in LDS; thread i < obs keeps
-// row i of A and B.  Activations pass through LDS with a barrier per layer.
-// Each output is one fma chain in ascending input order, which keeps the
-// result independent of the launch shape.
+// individual with all its weights in VGPRs for the whole episode.  The
+// summation order of every output (hidden layers: bias then inputs in order;
+// output layer: 8 slices folded pairwise, then the bias; dynamics: A s + B a)
+// is fixed, which keeps the result independent of the launch shape.
 //
 // The genotype is produced in the kernel's prologue straight from the parents
 // (or the Glorot-uniform first batch) -- offspring weights never touch HBM.
@@ -87,16 +86,25 @@ __device__ __forceinline__ void mlp_genes_run(const Params& p, const Pair& q, ui
   }
 }
 
+// One individual per workgroup of H threads (H / 64 waves):
+//   thread o      row o of W1 and W2, b1[o], b2[o] in VGPRs; hidden neuron o
+//   thread i < 27 row i of A and B (shared environment) in VGPRs; state i
+//   output wave   64 lanes (o3 = lane / 8, slice = lane % 8) hold W3[o3][slice
+//                 of H/8 inputs]; the 8 partial sums of an action are folded
+//                 inside its group of 8 lanes.  With H = 128 this is the second
+//                 wave, so the output layer and the dynamics run on different
+//                 waves.
+// Per step: layer 1 and the A s product, layer 2, output layer, B a product
+// and the new state; activations pass through LDS with one barrier per stage.
 template <int H, bool GEN0, bool KEEP>
 __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
-  constexpr int O = kObs, A = kAct;
-  constexpr int E1 = H * O, E2 = E1 + H, E3 = E2 + H * H, E4 = E3 + H;   // W3 at E4, b3 at E4 + A*H
+  constexpr int O = kObs, A = kAct, SL = H / 8;
+  constexpr int E1 = H * O, E2 = E1 + H, E3 = E2 + H * H, E4 = E3 + H;   // W3 at E4, b3 after
+  constexpr int OUT_WAVE_FIRST = H - 64;                                  // first lane of it
   __shared__ float s_state[2][32];
   __shared__ float s_h1[H];
   __shared__ float s_h2[H];
   __shared__ float s_a[A];
-  __shared__ float s_w3[A][H];
-  __shared__ float s_b3[A];
 
   const int o = threadIdx.x;
   const int j = blockIdx.x;
@@ -111,9 +119,11 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     q = select_pair(p, g, j, nocc);
   }
 
-  // ---- prologue: this individual's genotype, straight into registers / LDS
-  float w1[O], w2[H], arow[O], brow[A];
-  float b1v, b2v;
+  // ---- prologue: this individual's genotype, straight into registers
+  const bool out_lane = o >= OUT_WAVE_FIRST;
+  const int ol = o - OUT_WAVE_FIRST, o3 = (ol >> 3) & 7, slice = ol & 7;
+  float w1[O], w2[H], w3[SL], arow[O], brow[A];
+  float b1v, b2v, b3v = 0.0f;
   mlp_genes_run<GEN0, O>(p, q, g, j, o * O, w1);
   mlp_genes_aligned<GEN0, H>(p, q, g, j, E2 + o * H, w2);   // E2 = 28 H
   {
@@ -122,23 +132,22 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     b1v = t[0];
     mlp_genes_run<GEN0, 1>(p, q, g, j, E3 + o, t);
     b2v = t[0];
-  }
-  // W3 (A x H) and b3 (A): blocks shared out over the workgroup
-  for (int blk = (E4 >> 2) + o; blk < ((E4 + A * H + A) >> 2); blk += H) {
-    const float4 v = mlp_gene_block<GEN0>(p, q, g, j, blk);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int gi = 4 * blk + t - E4;
-      if (gi < A * H) s_w3[gi / H][gi % H] = pick4(v, t);
-      else s_b3[gi - A * H] = pick4(v, t);
+    if (out_lane) {
+      mlp_genes_run<GEN0, 1>(p, q, g, j, E4 + A * H + o3, t);
+      b3v = t[0];
     }
   }
+  if (out_lane) mlp_genes_aligned<GEN0, SL>(p, q, g, j, E4 + o3 * H + slice * SL, w3);
   if (KEEP) {
     float* row = p.off_geno + (size_t)j * (size_t)p.stride;
     for (int t = 0; t < O; ++t) row[o * O + t] = w1[t];
     for (int t = 0; t < H; ++t) row[E2 + o * H + t] = w2[t];
     row[E1 + o] = b1v;
     row[E3 + o] = b2v;
+    if (out_lane) {
+      for (int t = 0; t < SL; ++t) row[E4 + o3 * H + slice * SL + t] = w3[t];
+      if (slice == 0) row[E4 + A * H + o3] = b3v;
+    }
   }
   const float* envA = p.env;
   const float* envB = p.env + O * O;
@@ -151,11 +160,6 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     s_state[0][o] = envS[o];
   }
   __syncthreads();
-  if (KEEP) {
-    float* row = p.off_geno + (size_t)j * (size_t)p.stride;
-    for (int t = o; t < A * H; t += H) row[E4 + t] = s_w3[t / H][t % H];
-    if (o < A) row[E4 + A * H + o] = s_b3[o];
-  }
 
   // ---- episode
   float ret = 0.0f, dsum = 0.0f;
@@ -165,6 +169,11 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     float acc = b1v;
 #pragma unroll
     for (int k = 0; k < O; ++k) acc = fma32(w1[k], s[k], acc);
+    float as = 0.0f;
+    if (o < O) {
+#pragma unroll
+      for (int k = 0; k < O; ++k) as = fma32(arow[k], s[k], as);
+    }
     s_h1[o] = tanh32(acc);
     __syncthreads();
     acc = b2v;
@@ -172,20 +181,21 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     for (int k = 0; k < H; ++k) acc = fma32(w2[k], s_h1[k], acc);
     s_h2[o] = tanh32(acc);
     __syncthreads();
-    if (o < A) {
-      acc = s_b3[o];
+    if (out_lane) {
+      float pa = 0.0f;
 #pragma unroll
-      for (int k = 0; k < H; ++k) acc = fma32(s_w3[o][k], s_h2[k], acc);
-      s_a[o] = tanh32(acc);
+      for (int t = 0; t < SL; ++t) pa = fma32(w3[t], s_h2[slice * SL + t], pa);
+      pa = pa + __shfl_down(pa, 4, 8);   // slices s and s + 4
+      pa = pa + __shfl_down(pa, 2, 8);   // then s + 2
+      pa = pa + __shfl_down(pa, 1, 8);   // then s + 1
+      if (slice == 0) s_a[o3] = tanh32(pa + b3v);
     }
     __syncthreads();
     if (o < O) {
-      acc = 0.0f;
+      float ba = 0.0f;
 #pragma unroll
-      for (int k = 0; k < O; ++k) acc = fma32(arow[k], s[k], acc);
-#pragma unroll
-      for (int k = 0; k < A; ++k) acc = fma32(brow[k], s_a[k], acc);
-      const float sn = tanh32(acc);
+      for (int k = 0; k < A; ++k) ba = fma32(brow[k], s_a[k], ba);
+      const float sn = tanh32(as + ba);
       s_state[cur ^ 1][o] = sn;
       if (o == 0) {
         float qa = 0.0f;

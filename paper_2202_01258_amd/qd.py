@@ -130,16 +130,16 @@ def layout_query(cfg: QdConfig) -> QdLayout:
     return out
 
 
-def check_fast_arith(device: str = "cuda:0") -> int:
-    """Number of the 2^24 Box-Muller radius inputs where the short division /
-    square-root sequences differ from IEEE arithmetic (0 = identical)."""
+def check_fast_arith(device: str = "cuda:0") -> list:
+    """Mismatch counts of the short division / square-root sequences against
+    IEEE arithmetic: [radius (2^24 inputs), tanh (2^32), sigmoid (|x| <= 1)]."""
     import torch
-    scratch = torch.zeros(1, dtype=torch.int64, device=device)
-    out = C.c_uint64()
+    scratch = torch.zeros(3, dtype=torch.int64, device=device)
+    out = (C.c_uint64 * 3)()
     _check(lib().qd_check_fast_arith(C.c_void_p(scratch.data_ptr()),
-                                     C.c_void_p(_stream_handle(None)), C.byref(out)),
+                                     C.c_void_p(_stream_handle(None)), out),
            "qd_check_fast_arith")
-    return int(out.value)
+    return [int(v) for v in out]
 
 
 def _stream_handle(stream) -> int:
