@@ -313,18 +313,22 @@ int32_t or_cvt_cell(const float* d, int32_t D, const float* lo, const float* hi,
 /* output.  Genotype = [W1 (hid x obs), b1, W2 (hid x hid), b2, W3 (act x    */
 /* hid), b3], row-major.  Return = sum_t (s_{t+1}[0] - 0.5 |a_t|^2);          */
 /* descriptor k = mean over t = 1..T of sigmoid(s_t[k+1]), k = 0..3.          */
-/* Summation order: hidden layers take the bias, then their inputs in order.  */
-/* The output layer sums 8 contiguous slices of hid/8 inputs each, folds the  */
-/* 8 partial sums pairwise (s with s+4, then s+2, then s+1) and adds the bias. */
-/* The dynamics add the two products A s and B a, each summed in order.       */
+/* Summation order ("dot4"): input k goes to partial sum k mod 4, each an    */
+/* fma chain in input order from 0, folded as (p0 + p2) + (p1 + p3).  Hidden  */
+/* layers: tanh(dot4 + bias).  The output layer sums 8 contiguous slices of   */
+/* hid/8 inputs each (one chain each), folds the 8 partial sums pairwise (s   */
+/* with s+4, then s+2, then s+1) and adds the bias.  Dynamics:                */
+/* tanh(dot4(A row, s) + (B row . a in order)).                               */
 /* ------------------------------------------------------------------------ */
+static float dot4(const float* w, const float* x, int32_t n) {
+  float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int32_t k = 0; k < n; ++k) p[k & 3] = fmaf(w[k], x[k], p[k & 3]);
+  return (p[0] + p[2]) + (p[1] + p[3]);
+}
+
 static void dense_tanh(const float* W, const float* bias, const float* in, int32_t nin,
                        int32_t nout, float* out) {
-  for (int32_t o = 0; o < nout; ++o) {
-    float acc = bias[o];
-    for (int32_t k = 0; k < nin; ++k) acc = fmaf(W[(size_t)o * nin + k], in[k], acc);
-    out[o] = or_tanhf(acc);
-  }
+  for (int32_t o = 0; o < nout; ++o) out[o] = or_tanhf(dot4(W + (size_t)o * nin, in, nin) + bias[o]);
 }
 
 static void dense_tanh_sliced8(const float* W, const float* bias, const float* in, int32_t nin,
@@ -366,8 +370,8 @@ void or_mlp_rollout(const float* w, int32_t obs, int32_t hid, int32_t act, int32
     dense_tanh(W2, b2, h1, hid, hid, h2);
     dense_tanh_sliced8(W3, b3, h2, hid, act, a);
     for (int32_t i = 0; i < obs; ++i) {
-      float as = 0.0f, ba = 0.0f;
-      for (int32_t k = 0; k < obs; ++k) as = fmaf(A[(size_t)i * obs + k], s[k], as);
+      const float as = dot4(A + (size_t)i * obs, s, obs);
+      float ba = 0.0f;
       for (int32_t k = 0; k < act; ++k) ba = fmaf(B[(size_t)i * act + k], a[k], ba);
       sn[i] = or_tanhf(as + ba);
     }

@@ -7,9 +7,10 @@
 //
 // One workgroup of H threads (H = hidden width, one or two waves) runs one
 // individual with all its weights in VGPRs for the whole episode.  The
-// summation order of every output (hidden layers: bias then inputs in order;
-// output layer: 8 slices folded pairwise, then the bias; dynamics: A s + B a)
-// is fixed, which keeps the result independent of the launch shape.
+// summation order of every output is fixed (hidden layers and A s: four
+// interleaved partial sums, then the bias; output layer: 8 slices folded
+// pairwise, then the bias; dynamics: A s + B a), which keeps the result
+// independent of the launch shape.
 //
 // The genotype is produced in the kernel's prologue straight from the parents
 // (or the Glorot-uniform first batch) -- offspring weights never touch HBM.
@@ -50,6 +51,22 @@ __device__ __forceinline__ float4 mlp_gene_block(const Params& p, const Pair& q,
                        mlp_init_gene(p, i + 2, unit24(x.z)), mlp_init_gene(p, i + 3, unit24(x.w)));
   }
   return make_genes<false>(p, q, g, j, 4 * blk);
+}
+
+// Dot product in four interleaved partial sums (input k -> partial k mod 4,
+// each an fma chain in input order), folded as (p0 + p2) + (p1 + p3): four
+// independent dependency chains per lane.
+template <int N>
+__device__ __forceinline__ float dot4(const float* w, const float* x) {
+  float p0 = 0.0f, p1 = 0.0f, p2 = 0.0f, p3 = 0.0f;
+#pragma unroll
+  for (int k = 0; k < N; k += 4) {
+    p0 = fma32(w[k], x[k], p0);
+    if (k + 1 < N) p1 = fma32(w[k + 1], x[k + 1], p1);
+    if (k + 2 < N) p2 = fma32(w[k + 2], x[k + 2], p2);
+    if (k + 3 < N) p3 = fma32(w[k + 3], x[k + 3], p3);
+  }
+  return (p0 + p2) + (p1 + p3);
 }
 
 __device__ __forceinline__ float pick4(const float4& v, int k) {
@@ -166,20 +183,13 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   int cur = 0;
   for (int step = 0; step < p.T; ++step) {
     const float* s = s_state[cur];
-    float acc = b1v;
-#pragma unroll
-    for (int k = 0; k < O; ++k) acc = fma32(w1[k], s[k], acc);
+    const float z1 = dot4<O>(w1, s) + b1v;
     float as = 0.0f;
-    if (o < O) {
-#pragma unroll
-      for (int k = 0; k < O; ++k) as = fma32(arow[k], s[k], as);
-    }
-    s_h1[o] = tanh32(acc);
+    if (o < O) as = dot4<O>(arow, s);
+    s_h1[o] = tanh32(z1);
     __syncthreads();
-    acc = b2v;
-#pragma unroll
-    for (int k = 0; k < H; ++k) acc = fma32(w2[k], s_h1[k], acc);
-    s_h2[o] = tanh32(acc);
+    const float z2 = dot4<H>(w2, s_h1) + b2v;
+    s_h2[o] = tanh32(z2);
     __syncthreads();
     if (out_lane) {
       float pa = 0.0f;
