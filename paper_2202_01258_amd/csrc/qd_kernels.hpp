@@ -2,16 +2,18 @@
 //
 // Pipeline of one generation (Algorithm 1 after the first iteration; the
 // first iteration runs the same kernels with the random-init genotype):
-//   k_vary_eval   one wave64 per offspring: draw two parents uniformly from the
-//                 filled cells (Appendix A.2), Iso+LineDD (Algorithm 2) gene by
-//                 gene on coalesced float4 rows of both parents, the objective /
-//                 descriptor reduction (Appendix B.2).  Offspring genotypes are
-//                 not stored.  (Policies: k_rollout, same outputs.)
-//   k_insert      one thread per offspring: cell (grid bin, or exact nearest
-//                 CVT centroid through a bucket grid) and packed key; keys folded
-//                 per wave and per workgroup (LDS hash), at most one 64-bit
-//                 atomicMax per distinct cell per workgroup.
-//   k_regen       one wave per few cells: a cell whose key now names an
+//   k_vary_eval   a wave takes 4 offspring: draws their parents uniformly from
+//                 the filled cells (Appendix A.2), runs Iso+LineDD (Algorithm
+//                 2) gene by gene on coalesced float4 rows of both parents with
+//                 the objective / descriptor reduction (Appendix B.2) in the
+//                 same pass, then finds each offspring's cell (grid bin, or
+//                 exact nearest CVT centroid through a bucket grid) and inserts
+//                 its packed key with a 64-bit atomicMax that only offspring
+//                 beating the cell's current key issue.  Offspring genotypes
+//                 are not stored.
+//   k_rollout     (policies, qd_rollout.hpp) then k_insert: the same outputs;
+//                 keys folded per wave and per workgroup before the atomics.
+//   k_regen       a workgroup per few cells: a cell whose key now names an
 //                 offspring regenerates that offspring's genotype into the
 //                 cell's other genotype bank (the parents' banks were recorded
 //                 per offspring, so they stay readable), records objective and
@@ -330,92 +332,140 @@ __device__ __forceinline__ void record_empty_archive(const Params& p, int j) {
   atomicOr(reinterpret_cast<unsigned int*>(p.counters + 1), 1u);
 }
 
+// Inserts one packed key: an atomicMax on the cell's key, skipped when an
+// agent-scope read already shows a key at least as large (keys only grow),
+// so only offspring that beat everything seen so far reach the atomic unit.
+// An atomic that finds an empty cell raises the occupancy-changed flag.
+__device__ __forceinline__ void insert_one(const Params& p, int cell, uint64_t key) {
+  if (cell < 0) return;
+  unsigned long long* slot = (unsigned long long*)&p.arch_key[cell];
+  const unsigned long long cur = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (key <= cur) return;
+  if (atomicMax(slot, (unsigned long long)key) == 0ull) p.counters[3] = 1;
+}
+
 // ---------------------------------------------------------------------------
-// Select + vary + evaluate, one wave per offspring (test functions).
-// Lane l owns genes 256c + 4l .. 256c + 4l + 3 of every chunk c, i.e. gene
-// groups q = g/4 with q mod 64 = l; its partial sums run in ascending gene
-// order and the wave folds them pairwise (h = 32 .. 1).
+// Select + vary + evaluate + cell + insert (test functions).  A wave takes
+// kOffspringPerWave consecutive offspring: lanes 0..3 draw their parents
+// together, then the whole wave runs each offspring's genes in turn (lane l
+// owns genes 256c + 4l .. 256c + 4l + 3 of every chunk c, i.e. gene groups
+// q = g/4 with q mod 64 = l; its partial sums run in ascending gene order and
+// the wave folds them pairwise, h = 32 .. 1); finally lanes 0..3 find their
+// offspring's cell and insert its key.
 // ---------------------------------------------------------------------------
+constexpr int kOffspringPerWave = 4;
+
 template <int TASK, bool GEN0, bool KEEP>
 __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   const int lane = threadIdx.x & 63;
-  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (j >= p.nb) return;
+  const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kOffspringPerWave;
+  if (j0 >= p.nb) return;
+  const int nmine = p.nb - j0 < kOffspringPerWave ? p.nb - j0 : kOffspringPerWave;
+  const bool mine = lane < nmine;          // lane i speaks for offspring j0 + i
 
-  Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
+  Pair sel{nullptr, nullptr, 0.0f, -1, -1, 0u};
   if (!GEN0) {
     const int nocc = p.counters[0];
     if (nocc <= 0) {
-      if (lane == 0) record_empty_archive(p, j);
+      if (mine) record_empty_archive(p, j0 + lane);
       return;
     }
-    q = select_pair(p, g, j, nocc);
+    if (mine) sel = select_pair(p, g, j0 + lane, nocc);
   }
 
   const int n = p.n;
   const int half = n >> 1;
-  float acc = 0.0f, dlo = 0.0f, dhi = 0.0f;
-  float g0 = 0.0f, g1 = 0.0f;
-  float* keep_row = KEEP ? p.off_geno + (size_t)j * (size_t)p.stride : nullptr;
-  for (int base = 4 * lane; base < n; base += 256) {
-    const float4 v4 = make_genes<GEN0>(p, q, g, j, base);
-    if (KEEP) *reinterpret_cast<float4*>(keep_row + base) = v4;
-    if (base == 0) {
-      g0 = v4.x;
-      g1 = v4.y;
+  float my_f = 0.0f, my_d0 = 0.0f, my_d1 = 0.0f;
+  for (int i = 0; i < nmine; ++i) {
+    const int j = j0 + i;
+    Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
+    if (!GEN0) {
+      q.c1 = __shfl(sel.c1, i, 64);
+      q.c2 = __shfl(sel.c2, i, 64);
+      q.banks = (uint32_t)__shfl((int)sel.banks, i, 64);
+      q.lambda = __shfl(sel.lambda, i, 64);
+      q.row1 = geno_row(p, q.banks & 1u, q.c1);
+      q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
     }
-    if (base + 4 <= n) {
-      // whole block: the same additions in the same order, without per-gene tests
-      acc = acc + task_term<TASK>(v4.x);
-      acc = acc + task_term<TASK>(v4.y);
-      acc = acc + task_term<TASK>(v4.z);
-      acc = acc + task_term<TASK>(v4.w);
-      if (TASK == kTaskProj) {
-        if (base + 4 <= half) {
-          dlo = dlo + clip(v4.x, p.lo[0], p.hi[0]);
-          dlo = dlo + clip(v4.y, p.lo[0], p.hi[0]);
-          dlo = dlo + clip(v4.z, p.lo[0], p.hi[0]);
-          dlo = dlo + clip(v4.w, p.lo[0], p.hi[0]);
-        } else if (base >= half) {
-          dhi = dhi + clip(v4.x, p.lo[1], p.hi[1]);
-          dhi = dhi + clip(v4.y, p.lo[1], p.hi[1]);
-          dhi = dhi + clip(v4.z, p.lo[1], p.hi[1]);
-          dhi = dhi + clip(v4.w, p.lo[1], p.hi[1]);
-        } else {
-          const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+    float acc = 0.0f, dlo = 0.0f, dhi = 0.0f;
+    float g0 = 0.0f, g1 = 0.0f;
+    float* keep_row = KEEP ? p.off_geno + (size_t)j * (size_t)p.stride : nullptr;
+    for (int base = 4 * lane; base < n; base += 256) {
+      const float4 v4 = make_genes<GEN0>(p, q, g, j, base);
+      if (KEEP) *reinterpret_cast<float4*>(keep_row + base) = v4;
+      if (base == 0) {
+        g0 = v4.x;
+        g1 = v4.y;
+      }
+      if (base + 4 <= n) {
+        // whole block: the same additions in the same order, without per-gene tests
+        acc = acc + task_term<TASK>(v4.x);
+        acc = acc + task_term<TASK>(v4.y);
+        acc = acc + task_term<TASK>(v4.z);
+        acc = acc + task_term<TASK>(v4.w);
+        if (TASK == kTaskProj) {
+          if (base + 4 <= half) {
+            dlo = dlo + clip(v4.x, p.lo[0], p.hi[0]);
+            dlo = dlo + clip(v4.y, p.lo[0], p.hi[0]);
+            dlo = dlo + clip(v4.z, p.lo[0], p.hi[0]);
+            dlo = dlo + clip(v4.w, p.lo[0], p.hi[0]);
+          } else if (base >= half) {
+            dhi = dhi + clip(v4.x, p.lo[1], p.hi[1]);
+            dhi = dhi + clip(v4.y, p.lo[1], p.hi[1]);
+            dhi = dhi + clip(v4.z, p.lo[1], p.hi[1]);
+            dhi = dhi + clip(v4.w, p.lo[1], p.hi[1]);
+          } else {
+            const float v[4] = {v4.x, v4.y, v4.z, v4.w};
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            if (base + k < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
-            else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+            for (int k = 0; k < 4; ++k) {
+              if (base + k < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
+              else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+            }
+          }
+        }
+      } else {
+        // ragged last block
+        const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int gi = base + k;
+          if (gi < n) {
+            acc = acc + task_term<TASK>(v[k]);
+            if (TASK == kTaskProj) {
+              if (gi < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
+              else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
+            }
           }
         }
       }
+    }
+    // lane 0 holds the folded sums; lane i keeps offspring i's results
+    const float f = -__shfl(wave_fold_sum(acc), 0, 64);
+    float d0, d1;
+    if (TASK == kTaskProj) {
+      d0 = __shfl(wave_fold_sum(dlo), 0, 64) / (float)half;
+      d1 = __shfl(wave_fold_sum(dhi), 0, 64) / (float)(n - half);
     } else {
-      // ragged last block
-      const float v[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int gi = base + k;
-        if (gi < n) {
-          acc = acc + task_term<TASK>(v[k]);
-          if (TASK == kTaskProj) {
-            if (gi < half) dlo = dlo + clip(v[k], p.lo[0], p.hi[0]);
-            else dhi = dhi + clip(v[k], p.lo[1], p.hi[1]);
-          }
-        }
-      }
+      d0 = clip(__shfl(g0, 0, 64), p.lo[0], p.hi[0]);
+      d1 = clip(__shfl(g1, 0, 64), p.lo[1], p.hi[1]);
+    }
+    if (lane == i) {
+      my_f = f;
+      my_d0 = d0;
+      my_d1 = d1;
     }
   }
-  const float total = wave_fold_sum(acc);
-  float d[2];
-  if (TASK == kTaskProj) {
-    d[0] = wave_fold_sum(dlo) / (float)half;
-    d[1] = wave_fold_sum(dhi) / (float)(n - half);
-  } else {
-    d[0] = clip(g0, p.lo[0], p.hi[0]);
-    d[1] = clip(g1, p.lo[1], p.hi[1]);
+  if (mine) {
+    const int j = j0 + lane;
+    const float d[2] = {my_d0, my_d1};
+    const int cell = my_f == my_f ? (p.tess == kTessGrid ? grid_cell(p, d) : cvt_cell<2>(p, d))
+                                  : -1;
+    const uint64_t key = insert_key(p, my_f, cell, j);
+    record_offspring(p, j, sel, my_f, d);
+    p.off_cell[j] = cell;
+    p.off_key[j] = key;
+    insert_one(p, cell, key);
   }
-  if (lane == 0) record_offspring(p, j, q, -total, d);
 }
 
 // ---------------------------------------------------------------------------

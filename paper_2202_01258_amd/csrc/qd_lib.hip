@@ -195,7 +195,7 @@ unsigned blocks_for(uint64_t items, unsigned per_block) {
 template <bool GEN0>
 void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
-  const dim3 grid(blocks_for((uint64_t)p.nb, 4)), block(256);
+  const dim3 grid(blocks_for((uint64_t)p.nb, 4 * qd::kOffspringPerWave)), block(256);
   Timed t(h, s, QD_K_VARY_EVAL);
   const bool keep = h->cfg.keep_offspring != 0;
 #define QD_VE(TASK)                                                                      \
@@ -236,12 +236,14 @@ void launch_regen(qd_archive* h, hipStream_t s, uint32_t g) {
 template <bool GEN0>
 qd_status enqueue_generation(qd_archive* h, hipStream_t s, uint32_t g) {
   if (h->p.task == qd::kTaskMlp) {
-    Timed t(h, s, QD_K_ROLLOUT);
-    qd::launch_rollout(h->p, GEN0, g, h->cfg.keep_offspring != 0, s);
+    {
+      Timed t(h, s, QD_K_ROLLOUT);
+      qd::launch_rollout(h->p, GEN0, g, h->cfg.keep_offspring != 0, s);
+    }
+    launch_insert(h, s);
   } else {
-    launch_vary_eval<GEN0>(h, s, g);
+    launch_vary_eval<GEN0>(h, s, g);   // also finds cells and inserts
   }
-  launch_insert(h, s);
   launch_regen<GEN0>(h, s, g);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? QD_OK : hip_fail(e);
