@@ -13,7 +13,8 @@ Throughput `value` = N_B * K / (wall time of the K timed steps), bracketed by
 device synchronisation.  The paper's eval/s (mean over steps of N_B / t_n) is
 reported beside it from per-step HIP events.  The roofline object is for the
 dominant kernel, whose per-launch duration comes from HIP events that the
-library records around every launch on its stream during the timed steps.
+library records around each of its launches on its stream, over a second run
+of K steps right after the timed one.
 """
 from __future__ import annotations
 
@@ -130,9 +131,6 @@ def main():
     log(f"bench: {args.warmup} warmup steps done; timing {args.steps} steps")
 
     dominant = "rollout" if w["task"] == 3 else "vary_eval"
-    if not args.no_kernel_timing:
-        a.set_kernel_timing([dominant])     # events around the dominant kernel only
-        a.kernel_times()                    # clear
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -145,11 +143,19 @@ def main():
     t1 = time.perf_counter()
     wall = t1 - t0
     step_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
-    ktimes = a.kernel_times() if not args.no_kernel_timing else {}
-    # every kernel, in a separate pass of the same length (events between all
-    # launches cost a few microseconds each, so they stay out of the timed steps)
-    breakdown = {}
+    # The dominant kernel's launch duration: HIP events that the library records
+    # around each of its launches, over a second run of the same number of
+    # steps (events between kernels inside a step lengthen the step by several
+    # microseconds, so they stay out of the run that gives `value`); then
+    # every kernel, in a third run.
+    ktimes, breakdown = {}, {}
     if not args.no_kernel_timing:
+        a.set_kernel_timing([dominant])
+        a.kernel_times()
+        for _ in range(args.steps):
+            a.generation(g)
+            g += 1
+        ktimes = a.kernel_times()
         a.set_kernel_timing(["vary_eval", "rollout", "insert", "regen"])
         for _ in range(args.steps):
             a.generation(g)

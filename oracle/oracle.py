@@ -64,6 +64,8 @@ def lib():
             "or_philox_many": (None, [u32p, u32p, u32p, C.c_int64]),
             "or_box_muller_many": (None, [u32p, u32p, f32p, C.c_int64]),
             "or_turn_sincos_many": (None, [u32p, f32p, C.c_int64]),
+            "or_turn_sincos_tab_many": (None, [u32p, f32p, C.c_int64]),
+            "or_log_k24_many": (None, [u32p, f32p, C.c_int64]),
             "or_genotype_len": (C.c_int32, [C.POINTER(OrConfig)]),
             "or_env_len": (C.c_int32, [C.POINTER(OrConfig)]),
             "or_new": (P, [C.POINTER(OrConfig), C.c_int32]),
@@ -131,6 +133,20 @@ def turn_sincos(m) -> np.ndarray:
     m = np.ascontiguousarray(np.asarray(m, dtype=np.uint32).ravel())
     out = np.zeros((m.size, 2), dtype=np.float32)
     lib().or_turn_sincos_many(_ptr(m, C.c_uint32), _ptr(out, C.c_float), m.size)
+    return out
+
+
+def turn_sincos_tab(m) -> np.ndarray:
+    m = np.ascontiguousarray(np.asarray(m, dtype=np.uint32).ravel())
+    out = np.zeros((m.size, 2), dtype=np.float32)
+    lib().or_turn_sincos_tab_many(_ptr(m, C.c_uint32), _ptr(out, C.c_float), m.size)
+    return out
+
+
+def log_k24(k) -> np.ndarray:
+    k = np.ascontiguousarray(np.asarray(k, dtype=np.uint32).ravel())
+    out = np.zeros(k.size, dtype=np.float32)
+    lib().or_log_k24_many(_ptr(k, C.c_uint32), _ptr(out, C.c_float), k.size)
     return out
 
 

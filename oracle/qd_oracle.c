@@ -150,13 +150,79 @@ void or_turn_sincos(uint32_t m24, float out[2]) {
   out[1] = sn;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Table-driven forms used by the Gaussian sampler.  The tables are built    */
+/* from the functions above (so they hold the same bits on every machine):   */
+/*   turn table  T[i] = (cos, sin) of 2 pi i / 256, i = 0..255               */
+/*   log table   bin i of m in [1, 2) = [1 + i/128, 1 + (i+1)/128): a        */
+/*               reciprocal R_i of the bin's midpoint c_i and L_i; bins from */
+/*               53 up (m >= 1.4140625, about sqrt 2) move a factor 2 into   */
+/*               the exponent and take L_i = -ln(2 R_i), the others          */
+/*               L_i = -ln R_i.  The first bin uses R = 1 and the last       */
+/*               R = 1/2 with L = 0, so that logs near 1 come out without    */
+/*               cancellation.                                               */
+/* ------------------------------------------------------------------------ */
+static float g_turn[256][2];
+static float g_logr[128], g_logl[128];
+static int g_tables_built = 0;
+
+static void build_tables(void) {
+  if (g_tables_built) return;
+  for (uint32_t i = 0; i < 256; ++i) or_turn_sincos(i << 16, g_turn[i]);
+  for (int i = 0; i < 128; ++i) {
+    if (i == 0) { g_logr[i] = 1.0f; g_logl[i] = 0.0f; continue; }
+    if (i == 127) { g_logr[i] = 0.5f; g_logl[i] = 0.0f; continue; }
+    float c = 1.0f + ((float)i + 0.5f) / 128.0f;       /* exact */
+    float r = 1.0f / c;                                 /* IEEE division */
+    g_logr[i] = r;
+    g_logl[i] = -or_logf(i >= 53 ? r + r : r);
+  }
+  g_tables_built = 1;
+}
+
+/* cos and sin of 2 pi m / 2^24 (24-bit m) from the turn table: angle =
+ * 2 pi (m >> 16) / 256 + delta, delta = (m & 0xffff) (2 pi 2^-24) in [0, 2 pi/256),
+ * sin delta ~ delta - delta^3/6, cos delta ~ 1 - delta^2/2 + delta^4/24,
+ * then the angle-addition formulas. */
+void or_turn_sincos_tab(uint32_t m24, float out[2]) {
+  build_tables();
+  uint32_t m = m24 & 0xffffffu;
+  const float* t = g_turn[m >> 16];
+  float d = (float)(m & 0xffffu) * (kPi * 0x1p-23f);
+  float d2 = d * d;
+  float sd = fmaf(d * d2, -1.0f / 6.0f, d);
+  float cd = fmaf(d2, fmaf(d2, 1.0f / 24.0f, -0.5f), 1.0f);
+  out[0] = fmaf(t[0], cd, -(t[1] * sd));
+  out[1] = fmaf(t[1], cd, t[0] * sd);
+}
+
+/* ln(k 2^-24) for an integer k in [1, 2^24] from the log table: k = 2^E m,
+ * m in [1, 2), bin i = top 7 fraction bits of m, t = m R_i - 1 (one rounding),
+ * ln(m 2^-f) = L_i + t - t^2/2 + t^3/3 - t^4/4 with f = 1 for bins i >= 53
+ * (else 0), and exponent E - 24 + f. */
+float or_log_k24(uint32_t k) {
+  build_tables();
+  float kf = (float)k;
+  uint32_t b = f2u(kf);
+  int e = (int)(b >> 23) - 127 - 24;
+  uint32_t i = (b >> 16) & 0x7fu;
+  if (i >= 53u) e += 1;
+  float m = u2f((b & 0x7fffffu) | 0x3f800000u);
+  float t = fmaf(m, g_logr[i], -1.0f);
+  float q = fmaf(t, -0.25f, 1.0f / 3.0f);
+  q = fmaf(t, q, -0.5f);
+  float lnm = g_logl[i] + fmaf(t * t, q, t);
+  float fe = (float)e;
+  return fmaf(fe, kLn2Hi, fmaf(fe, kLn2Lo, lnm));
+}
+
 /* Box-Muller (1958): two standard normals from two Philox words.  The radius
- * uses the (0,1] uniform so ln never sees 0; the angle uses the top 24 bits. */
+ * uses the (0,1] uniform ((xa >> 8) + 1) 2^-24 so ln never sees 0; the angle
+ * uses the top 24 bits of xb. */
 void or_box_muller(uint32_t xa, uint32_t xb, float out[2]) {
-  float u1 = or_u24p(xa);
-  float r = sqrtf(-2.0f * or_logf(u1));
+  float r = sqrtf(-2.0f * or_log_k24((xa >> 8) + 1u));
   float cs[2];
-  or_turn_sincos(xb >> 8, cs);
+  or_turn_sincos_tab(xb >> 8, cs);
   out[0] = r * cs[0];
   out[1] = r * cs[1];
 }
@@ -729,4 +795,12 @@ void or_box_muller_many(const uint32_t* xa, const uint32_t* xb, float* out, int6
 
 void or_turn_sincos_many(const uint32_t* m, float* out, int64_t count) {
   for (int64_t i = 0; i < count; ++i) or_turn_sincos(m[i], out + 2 * i);
+}
+
+void or_turn_sincos_tab_many(const uint32_t* m, float* out, int64_t count) {
+  for (int64_t i = 0; i < count; ++i) or_turn_sincos_tab(m[i], out + 2 * i);
+}
+
+void or_log_k24_many(const uint32_t* k, float* out, int64_t count) {
+  for (int64_t i = 0; i < count; ++i) out[i] = or_log_k24(k[i]);
 }

@@ -64,6 +64,10 @@ void     or_philox_many(const uint32_t* ctr, const uint32_t key[2], uint32_t* ou
 void     or_box_muller_many(const uint32_t* xa, const uint32_t* xb, float* out,
                             int64_t count);
 void     or_turn_sincos_many(const uint32_t* m, float* out, int64_t count);
+void     or_turn_sincos_tab(uint32_t m24, float out[2]);
+float    or_log_k24(uint32_t k);
+void     or_turn_sincos_tab_many(const uint32_t* m, float* out, int64_t count);
+void     or_log_k24_many(const uint32_t* k, float* out, int64_t count);
 
 /* ---- the run ---- */
 int32_t   or_genotype_len(const or_config* cfg);

@@ -68,22 +68,13 @@ constexpr float kPi = 0x1.921fb6p+1f;
 constexpr float kHalfPi = 0x1.921fb6p+0f;
 constexpr float kLog2e = 0x1.715476p+0f;
 
-// Quotient a / b for b in [1.7, 2.5] (so no scaling is ever needed):
-// hardware reciprocal, product, one residual correction.  On the inputs the
-// logarithm below can see it returns the IEEE quotient bit for bit; the library
-// checks that over all of them (qd_check_fast_arith).
-__device__ __forceinline__ float div_narrow(float a, float b) {
-  const float y = __builtin_amdgcn_rcpf(b);
-  const float q = a * y;
-  const float r = fma32(-q, b, a);
-  return fma32(r, y, q);
-}
-
 // Square root of a positive normal x (or +-0) without the small-input
 // scaling: hardware estimate, then the neighbour one unit in the last place
 // below or above is taken when the fma residual says the estimate rounded
 // the wrong way.  (For x = +-0 both neighbours fail their test, so +-0 comes
-// back unchanged.)  Checked against IEEE sqrt like div_narrow.
+// back unchanged.)  On every input the Box-Muller radius can feed it this
+// returns the IEEE square root bit for bit; the library checks that over all
+// of them (qd_check_fast_arith).
 __device__ __forceinline__ float sqrt_normal(float x) {
   const float s = __builtin_amdgcn_sqrtf(x);
   const float dn = __uint_as_float(__float_as_uint(s) - 1u);
@@ -92,19 +83,16 @@ __device__ __forceinline__ float sqrt_normal(float x) {
   return fma32(-up, s, x) > 0.0f ? up : r;
 }
 
-// ln (x 2^-scale) for positive normal x.  x = 2^e m, m folded into
-// [sqrt(1/2), sqrt(2)); ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd
-// series through s^9.  FAST selects div_narrow for the quotient; both give
-// the same bits.  (A power-of-two factor only moves the exponent, so passing
-// it as `scale` gives the bits of log_pos(x * 2^-scale).)
-template <bool FAST = false>
-__device__ __forceinline__ float log_pos(float x, int scale = 0) {
+// ln x for positive normal x.  x = 2^e m, m folded into [sqrt(1/2), sqrt(2));
+// ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd series through s^9.  Used
+// to fill the log table of the Gaussian sampler.
+__device__ __forceinline__ float log_pos(float x) {
   const uint32_t bits = __float_as_uint(x);
   const uint32_t frac = bits & 0x7fffffu;
   const bool fold = frac > 0x3504f3u;
-  const int e = (int)(bits >> 23) - (127 + scale) + (fold ? 1 : 0);
+  const int e = (int)(bits >> 23) - 127 + (fold ? 1 : 0);
   const float m = __uint_as_float((frac | 0x3f800000u) - (fold ? 0x00800000u : 0u));
-  const float s = FAST ? div_narrow(m - 1.0f, m + 1.0f) : (m - 1.0f) / (m + 1.0f);
+  const float s = (m - 1.0f) / (m + 1.0f);
   const float s2 = s * s;
   float p = fma32(s2, 2.0f / 9.0f, 2.0f / 7.0f);
   p = fma32(s2, p, 2.0f / 5.0f);
@@ -150,22 +138,82 @@ __device__ __forceinline__ float2 turn_cos_sin(uint32_t m) {
                      __uint_as_float(__float_as_uint(b) ^ flip_sin));
 }
 
-// Box-Muller radius sqrt(-2 ln u1), u1 the (0,1] uniform of word xa: with
-// IEEE division and square root, and with the short sequences (FAST).
-__device__ __forceinline__ float bm_radius_ieee(uint32_t xa) {
-  return __builtin_sqrtf(-2.0f * log_pos<false>(unit24_open0(xa)));
+// ---------------------------------------------------------------------------
+// Table-driven forms for the Gaussian sampler.  Each workgroup builds the two
+// small tables in LDS from the functions above, so they hold the same bits
+// everywhere:
+//   turn[i] = (cos, sin) of 2 pi i / 256 (turn_cos_sin at i << 16)
+//   logt[i] = (R_i, L_i) for bin i of m in [1, 2) ([1 + i/128, 1 + (i+1)/128)):
+//             R_i = 1 / c_i (IEEE division, c_i the bin's midpoint) and
+//             L_i = -ln R_i, or -ln(2 R_i) with a factor 2 moved into the
+//             exponent for bins from 53 up (m >= 1.4140625); bin 0 uses R = 1
+//             and bin 127 R = 1/2, with L = 0, so logs near 1 do not cancel.
+// ---------------------------------------------------------------------------
+struct Tables {
+  const float2* turn;   // [256]
+  const float2* logt;   // [128]
+};
+
+__device__ __forceinline__ void build_tables(float2* turn, float2* logt, int tid, int nthreads) {
+  for (int i = tid; i < 256; i += nthreads) turn[i] = turn_cos_sin((uint32_t)i << 16);
+  for (int i = tid; i < 128; i += nthreads) {
+    float r = 1.0f, l = 0.0f;
+    if (i == 127) {
+      r = 0.5f;
+    } else if (i > 0) {
+      const float c = 1.0f + ((float)i + 0.5f) / 128.0f;
+      r = 1.0f / c;
+      l = -log_pos(i >= 53 ? r + r : r);
+    }
+    logt[i] = make_float2(r, l);
+  }
 }
-__device__ __forceinline__ float bm_radius(uint32_t xa) {
-  // unit24_open0(xa) = ((xa >> 8) + 1) 2^-24: the 2^-24 goes to the exponent
-  return sqrt_normal(-2.0f * log_pos<true>((float)((xa >> 8) + 1u), 24));
+
+// cos and sin of 2 pi m / 2^24 from the turn table and the remainder
+// delta = (m & 0xffff) 2 pi 2^-24: sin delta ~ delta - delta^3/6,
+// cos delta ~ 1 - delta^2/2 + delta^4/24, angle-addition formulas.
+__device__ __forceinline__ float2 turn_tab(uint32_t m, const Tables& tb) {
+  const float2 t = tb.turn[m >> 16];
+  const float d = (float)(m & 0xffffu) * (kPi * 0x1p-23f);
+  const float d2 = d * d;
+  const float sd = fma32(d * d2, -1.0f / 6.0f, d);
+  const float cd = fma32(d2, fma32(d2, 1.0f / 24.0f, -0.5f), 1.0f);
+  return make_float2(fma32(t.x, cd, -(t.y * sd)), fma32(t.y, cd, t.x * sd));
+}
+
+// ln(k 2^-24), integer k in [1, 2^24]: k = 2^E m, bin i = top 7 fraction bits
+// of m, t = m R_i - 1 in one rounding, ln(m 2^-f) = L_i + t - t^2/2 + t^3/3
+// - t^4/4 (f = 1 for bins from 53 up), exponent E - 24 + f.
+__device__ __forceinline__ float log_k24(uint32_t k, const Tables& tb) {
+  const uint32_t b = __float_as_uint((float)k);
+  const uint32_t i = (b >> 16) & 0x7fu;
+  const int e = (int)(b >> 23) - (127 + 24) + (i >= 53u ? 1 : 0);
+  const float m = __uint_as_float((b & 0x7fffffu) | 0x3f800000u);
+  const float2 rl = tb.logt[i];
+  const float t = fma32(m, rl.x, -1.0f);
+  float q = fma32(t, -0.25f, 1.0f / 3.0f);
+  q = fma32(t, q, -0.5f);
+  const float lnm = rl.y + fma32(t * t, q, t);
+  const float fe = (float)e;
+  return fma32(fe, kLn2Hi, fma32(fe, kLn2Lo, lnm));
+}
+
+// Box-Muller radius sqrt(-2 ln u1), u1 = ((xa >> 8) + 1) 2^-24: with the IEEE
+// square root, and with the short sequence the kernels use.
+__device__ __forceinline__ float bm_radius_ieee(uint32_t xa, const Tables& tb) {
+  return __builtin_sqrtf(-2.0f * log_k24((xa >> 8) + 1u, tb));
+}
+__device__ __forceinline__ float bm_radius(uint32_t xa, const Tables& tb) {
+  return sqrt_normal(-2.0f * log_k24((xa >> 8) + 1u, tb));
 }
 
 // Two standard normals (Box-Muller) from two Philox words.
-__device__ __forceinline__ float2 gauss2(uint32_t xa, uint32_t xb) {
-  const float r = bm_radius(xa);
-  const float2 cs = turn_cos_sin(xb >> 8);
+__device__ __forceinline__ float2 gauss2(uint32_t xa, uint32_t xb, const Tables& tb) {
+  const float r = bm_radius(xa, tb);
+  const float2 cs = turn_tab(xb >> 8, tb);
   return make_float2(r * cs.x, r * cs.y);
 }
+
 
 // sin(pi x) up to sign: r = x - rint(x) (exact), y = pi r, Taylor to y^13.
 __device__ __forceinline__ float sinpi_unsigned(float x) {
@@ -243,11 +291,31 @@ __device__ __forceinline__ float sigmoid32(float x) {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
-// Pairwise fold of one value per lane: after the steps h = 32, 16, ..., 1
-// (lane l adds lane l + h), lane 0 holds the total in that fixed order.
+// Pairwise fold of one value per lane in the fixed tree h = 32, 16, ..., 1
+// (the partial of lane l is added to that of lane l + h), without LDS: the
+// steps h = 32 and 16 exchange halves and rows with the lane-swap
+// instructions, h = 8 .. 1 rotate within rows of 16 lanes (DPP).  Every step
+// leaves each lane holding its pair's sum (addition commutes, so both members
+// of a pair hold the same bits), and the total ends in every lane.
+// DPP within rows of 16 lanes: row_shl<N> gives lane l the value of lane
+// l + N (0 past the row's end), row_ror<N> that of lane (l - N) mod 16.
+template <int N>
+__device__ __forceinline__ float row_shl(float v) {
+  return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x100 + N, 0xf, 0xf, false));
+}
+template <int N>
+__device__ __forceinline__ float row_ror(float v) {
+  return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x120 + N, 0xf, 0xf, false));
+}
 __device__ __forceinline__ float wave_fold_sum(float v) {
-#pragma unroll
-  for (int h = 32; h >= 1; h >>= 1) v = v + __shfl_down(v, h, 64);
+  const auto h32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(h32[0]) + __uint_as_float(h32[1]);
+  const auto h16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(h16[0]) + __uint_as_float(h16[1]);
+  v = v + row_ror<8>(v);
+  v = v + row_ror<4>(v);
+  v = v + row_ror<2>(v);
+  v = v + row_ror<1>(v);
   return v;
 }
 

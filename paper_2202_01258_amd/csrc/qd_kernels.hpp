@@ -77,14 +77,17 @@ struct Pair {
   float lambda;
   int c1, c2;
   uint32_t banks;
+  Tables tb;                      // the workgroup's sampler tables (LDS)
 };
 
-__device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, int nocc) {
+__device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, int nocc,
+                                            const Tables& tb) {
   const uint4 x = philox(0u, (uint32_t)j, g, kTagSelect, p.key);
   Pair q;
   q.c1 = pick(p.occ_list, x.x, nocc);
   q.c2 = pick(p.occ_list, x.y, nocc);
-  q.lambda = p.line_sigma * gauss2(x.z, x.w).x;
+  q.tb = tb;
+  q.lambda = p.line_sigma * gauss2(x.z, x.w, tb).x;
   const uint32_t b1 = p.arch_slot[q.c1], b2 = p.arch_slot[q.c2];
   q.banks = b1 | (b2 << 1);
   q.row1 = geno_row(p, b1, q.c1);
@@ -94,13 +97,15 @@ __device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, 
 
 // The same pair, rebuilt after the generation from what the offspring
 // recorded (cells and banks) -- independent of the archive's current state.
-__device__ __forceinline__ Pair recorded_pair(const Params& p, uint32_t g, int j) {
+__device__ __forceinline__ Pair recorded_pair(const Params& p, uint32_t g, int j,
+                                              const Tables& tb) {
   const uint4 x = philox(0u, (uint32_t)j, g, kTagSelect, p.key);
   Pair q;
   q.c1 = p.off_par[2 * j];
   q.c2 = p.off_par[2 * j + 1];
   q.banks = p.off_bank[j];
-  q.lambda = p.line_sigma * gauss2(x.z, x.w).x;
+  q.tb = tb;
+  q.lambda = p.line_sigma * gauss2(x.z, x.w, tb).x;
   q.row1 = geno_row(p, q.banks & 1u, q.c1);
   q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
   return q;
@@ -122,8 +127,8 @@ __device__ __forceinline__ float4 make_genes(const Params& p, const Pair& q, uin
     const float4 t1 = *reinterpret_cast<const float4*>(q.row1 + base);
     const float4 t2 = *reinterpret_cast<const float4*>(q.row2 + base);
     const uint4 x = philox((uint32_t)(base >> 2), (uint32_t)j, g, kTagIso, p.key);
-    const float2 e01 = gauss2(x.x, x.y);
-    const float2 e23 = gauss2(x.z, x.w);
+    const float2 e01 = gauss2(x.x, x.y, q.tb);
+    const float2 e23 = gauss2(x.z, x.w, q.tb);
     const float s1 = p.iso_sigma, l = q.lambda;
     return make_float4(fma32(l, t2.x - t1.x, fma32(s1, e01.x, t1.x)),
                        fma32(l, t2.y - t1.y, fma32(s1, e01.y, t1.y)),
@@ -357,6 +362,12 @@ constexpr int kOffspringPerWave = 4;
 
 template <int TASK, bool GEN0, bool KEEP>
 __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
+  __shared__ float2 s_turn[256], s_logt[128];
+  if (!GEN0) {
+    build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
+    __syncthreads();
+  }
+  const Tables tb{s_turn, s_logt};
   const int lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kOffspringPerWave;
   if (j0 >= p.nb) return;
@@ -370,7 +381,7 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
       if (mine) record_empty_archive(p, j0 + lane);
       return;
     }
-    if (mine) sel = select_pair(p, g, j0 + lane, nocc);
+    if (mine) sel = select_pair(p, g, j0 + lane, nocc, tb);
   }
 
   const int n = p.n;
@@ -378,7 +389,7 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   float my_f = 0.0f, my_d0 = 0.0f, my_d1 = 0.0f;
   for (int i = 0; i < nmine; ++i) {
     const int j = j0 + i;
-    Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
+    Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u, tb};
     if (!GEN0) {
       q.c1 = __shfl(sel.c1, i, 64);
       q.c2 = __shfl(sel.c2, i, 64);
@@ -439,15 +450,15 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
         }
       }
     }
-    // lane 0 holds the folded sums; lane i keeps offspring i's results
-    const float f = -__shfl(wave_fold_sum(acc), 0, 64);
+    // every lane gets the folded sums; lane i keeps offspring i's results
+    const float f = -wave_fold_sum(acc);
     float d0, d1;
     if (TASK == kTaskProj) {
-      d0 = __shfl(wave_fold_sum(dlo), 0, 64) / (float)half;
-      d1 = __shfl(wave_fold_sum(dhi), 0, 64) / (float)(n - half);
+      d0 = wave_fold_sum(dlo) / (float)half;
+      d1 = wave_fold_sum(dhi) / (float)(n - half);
     } else {
-      d0 = clip(__shfl(g0, 0, 64), p.lo[0], p.hi[0]);
-      d1 = clip(__shfl(g1, 0, 64), p.lo[1], p.hi[1]);
+      d0 = clip(__uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g0), 0)), p.lo[0], p.hi[0]);
+      d1 = clip(__uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g1), 0)), p.lo[1], p.hi[1]);
     }
     if (lane == i) {
       my_f = f;
@@ -613,6 +624,32 @@ __device__ __forceinline__ bool names_offspring(uint64_t key) {
   return key != 0ull && (uint32_t)key != 0xffffffffu;
 }
 
+// Copies the keys of the workgroup's cells first .. first + kRegenCells - 1
+// into LDS (0 past the archive's end) and returns whether any names an
+// offspring of this batch (the same answer in every thread).  Every thread
+// must call it.
+__device__ __forceinline__ bool stage_keys(const Params& p, int first, uint64_t* s_key) {
+  if (threadIdx.x < kRegenCells) {
+    const int c = first + (int)threadIdx.x;
+    s_key[threadIdx.x] = c < p.C ? p.arch_key[c] : 0ull;
+  }
+  __syncthreads();
+  bool any = false;
+#pragma unroll
+  for (int t = 0; t < kRegenCells; ++t) any |= names_offspring(s_key[t]);
+  return any;
+}
+
+// After the genotypes are written: the winners' cells take objective,
+// descriptor, bank and incumbent key.
+__device__ __forceinline__ void finish_cells(const Params& p, int first, const uint64_t* s_key) {
+  __syncthreads();
+  if (threadIdx.x < kRegenCells) {
+    const uint64_t key = s_key[threadIdx.x];
+    if (names_offspring(key)) finish_winner(p, first + (int)threadIdx.x, p.nb - 1 - (int)(uint32_t)key, key);
+  }
+}
+
 // Workgroups 0 .. ceil(C / kRegenCells) - 1 take cells; one more compacts.
 inline unsigned regen_blocks(int C) { return (unsigned)((C + kRegenCells - 1) / kRegenCells) + 1u; }
 
@@ -624,24 +661,26 @@ __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int first = blockIdx.x * kRegenCells;
-  for (int c = first; c < first + kRegenCells && c < p.C; ++c) {
-    const uint64_t key = p.arch_key[c];
+  __shared__ uint64_t s_key[kRegenCells];
+  __shared__ float2 s_turn[256], s_logt[128];
+  if (!stage_keys(p, first, s_key)) return;
+  if (!GEN0) {
+    build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
+    __syncthreads();
+  }
+  const Tables tb{s_turn, s_logt};
+  for (int t = 0; t < kRegenCells; ++t) {
+    const uint64_t key = s_key[t];
     if (!names_offspring(key)) continue;
+    const int c = first + t;
     const int j = p.nb - 1 - (int)(uint32_t)key;
     Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
-    if (!GEN0) q = recorded_pair(p, g, j);
+    if (!GEN0) q = recorded_pair(p, g, j, tb);
     float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
     for (int base = 256 * wave + 4 * lane; base < p.n; base += 1024)
       *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
   }
-  __syncthreads();
-  if (threadIdx.x < kRegenCells) {
-    const int c = first + threadIdx.x;
-    if (c < p.C) {
-      const uint64_t key = p.arch_key[c];
-      if (names_offspring(key)) finish_winner(p, c, p.nb - 1 - (int)(uint32_t)key, key);
-    }
-  }
+  finish_cells(p, first, s_key);
 }
 
 // ---------------------------------------------------------------------------
@@ -776,10 +815,14 @@ __global__ void k_bucket_fill(const Params p) {
 
 // Entry e of [A | B | s0] = 0.1 * normal (e mod 4) of block (e/4, 0, 0, ENV).
 __global__ void k_env(const Params p, int count) {
+  __shared__ float2 s_turn[256], s_logt[128];
+  build_tables(s_turn, s_logt, (int)threadIdx.x, (int)blockDim.x);
+  __syncthreads();
+  const Tables tb{s_turn, s_logt};
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (4 * b >= count) return;
   const uint4 x = philox((uint32_t)b, 0u, 0u, kTagEnv, p.key);
-  const float2 z01 = gauss2(x.x, x.y), z23 = gauss2(x.z, x.w);
+  const float2 z01 = gauss2(x.x, x.y, tb), z23 = gauss2(x.z, x.w, tb);
   const float z[4] = {z01.x, z01.y, z23.x, z23.y};
   for (int k = 0; k < 4; ++k)
     if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
@@ -798,12 +841,16 @@ __device__ __forceinline__ bool same_bits(float a, float b) {
 }
 
 __global__ __launch_bounds__(256) void k_check_fast(unsigned long long* count) {
+  __shared__ float2 s_turn[256], s_logt[128];
+  build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
+  __syncthreads();
+  const Tables tb{s_turn, s_logt};
   const uint64_t nthr = (uint64_t)gridDim.x * blockDim.x;
   const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   unsigned long long bad_r = 0, bad_t = 0, bad_s = 0;
   for (uint64_t k = tid; k < (1ull << 24); k += nthr) {
     const uint32_t xa = (uint32_t)k << 8;
-    bad_r += same_bits(bm_radius(xa), bm_radius_ieee(xa)) ? 0 : 1;
+    bad_r += same_bits(bm_radius(xa, tb), bm_radius_ieee(xa, tb)) ? 0 : 1;
   }
   for (uint64_t k = tid; k < (1ull << 32); k += nthr) {
     const float x = __uint_as_float((uint32_t)k);

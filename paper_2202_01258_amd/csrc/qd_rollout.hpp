@@ -53,6 +53,14 @@ __device__ __forceinline__ float4 mlp_gene_block(const Params& p, const Pair& q,
   return make_genes<false>(p, q, g, j, 4 * blk);
 }
 
+// Makes the four genes opaque to the optimiser (an empty asm that claims to
+// change them): the prologue's genes are then finished where they are made,
+// instead of having the sampler's inputs carried into the episode loop where
+// the genes are first read, which needs several times the registers.
+__device__ __forceinline__ void settle(float4& v) {
+  __asm__ volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+}
+
 // Dot product in four interleaved partial sums (input k -> partial k mod 4,
 // each an fma chain in input order), folded as (p0 + p2) + (p1 + p3): four
 // independent dependency chains per lane.
@@ -80,7 +88,8 @@ __device__ __forceinline__ void mlp_genes_aligned(const Params& p, const Pair& q
   static_assert(LEN % 4 == 0, "aligned runs hold whole gene blocks");
 #pragma unroll
   for (int t4 = 0; t4 < LEN / 4; ++t4) {
-    const float4 v = mlp_gene_block<GEN0>(p, q, g, j, (first >> 2) + t4);
+    float4 v = mlp_gene_block<GEN0>(p, q, g, j, (first >> 2) + t4);
+    settle(v);
     dst[4 * t4] = v.x;
     dst[4 * t4 + 1] = v.y;
     dst[4 * t4 + 2] = v.z;
@@ -94,7 +103,8 @@ __device__ __forceinline__ void mlp_genes_run(const Params& p, const Pair& q, ui
                                               int first, float* dst) {
   const int b0 = first >> 2, b1 = (first + LEN - 1) >> 2;
   for (int blk = b0; blk <= b1; ++blk) {
-    const float4 v = mlp_gene_block<GEN0>(p, q, g, j, blk);
+    float4 v = mlp_gene_block<GEN0>(p, q, g, j, blk);
+    settle(v);
 #pragma unroll
     for (int t = 0; t < LEN; ++t) {
       const int gi = first + t;
@@ -123,6 +133,8 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   __shared__ float s_h2[H];
   __shared__ float s_a[A];
 
+  __shared__ float2 s_turn[256], s_logt[128];
+
   const int o = threadIdx.x;
   const int j = blockIdx.x;
 
@@ -133,7 +145,9 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
       if (o == 0) record_empty_archive(p, j);
       return;
     }
-    q = select_pair(p, g, j, nocc);
+    build_tables(s_turn, s_logt, o, H);
+    __syncthreads();
+    q = select_pair(p, g, j, nocc, Tables{s_turn, s_logt});
   }
 
   // ---- prologue: this individual's genotype, straight into registers
@@ -195,9 +209,9 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
       float pa = 0.0f;
 #pragma unroll
       for (int t = 0; t < SL; ++t) pa = fma32(w3[t], s_h2[slice * SL + t], pa);
-      pa = pa + __shfl_down(pa, 4, 8);   // slices s and s + 4
-      pa = pa + __shfl_down(pa, 2, 8);   // then s + 2
-      pa = pa + __shfl_down(pa, 1, 8);   // then s + 1
+      pa = pa + row_shl<4>(pa);   // slices s and s + 4 (groups of 8 never straddle a row)
+      pa = pa + row_shl<2>(pa);   // then s + 2
+      pa = pa + row_shl<1>(pa);   // then s + 1
       if (slice == 0) s_a[o3] = tanh32(pa + b3v);
     }
     __syncthreads();
@@ -241,24 +255,26 @@ __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
   const int tid = threadIdx.x;
   const int first = blockIdx.x * kRegenCells;
   const int nblk = (p.n + 3) >> 2;
-  for (int c = first; c < first + kRegenCells && c < p.C; ++c) {
-    const uint64_t key = p.arch_key[c];
+  __shared__ uint64_t s_key[kRegenCells];
+  __shared__ float2 s_turn[256], s_logt[128];
+  if (!stage_keys(p, first, s_key)) return;
+  if (!GEN0) {
+    build_tables(s_turn, s_logt, tid, 256);
+    __syncthreads();
+  }
+  const Tables tb{s_turn, s_logt};
+  for (int t = 0; t < kRegenCells; ++t) {
+    const uint64_t key = s_key[t];
     if (!names_offspring(key)) continue;
+    const int c = first + t;
     const int j = p.nb - 1 - (int)(uint32_t)key;
     Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
-    if (!GEN0) q = recorded_pair(p, g, j);
+    if (!GEN0) q = recorded_pair(p, g, j, tb);
     float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
     for (int blk = tid; blk < nblk; blk += 256)
       *reinterpret_cast<float4*>(dst + 4 * blk) = mlp_gene_block<GEN0>(p, q, g, j, blk);
   }
-  __syncthreads();
-  if (tid < kRegenCells) {
-    const int c = first + tid;
-    if (c < p.C) {
-      const uint64_t key = p.arch_key[c];
-      if (names_offspring(key)) finish_winner(p, c, p.nb - 1 - (int)(uint32_t)key, key);
-    }
-  }
+  finish_cells(p, first, s_key);
 }
 
 inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hipStream_t s) {

@@ -26,6 +26,18 @@ def test_log_exhaustive_on_box_muller_domain():
     assert ulp_err(got[ok], ref[ok]).max() <= 3.0
 
 
+def test_table_log_exhaustive_on_box_muller_domain():
+    # the table-driven ln(k 2^-24) the sampler uses, for every k = 1..2^24
+    k = np.arange(1, (1 << 24) + 1, dtype=np.uint32)
+    got = O.log_k24(k)
+    ref = np.log(k.astype(np.float64) / 2.0**24)
+    ok = ref != 0
+    assert got[~ok].tolist() == [0.0]
+    assert ulp_err(got[ok], ref[ok]).max() <= 2.5
+    # monotone in k: a property any reordering of bins or sign slip breaks
+    assert np.all(np.diff(got.astype(np.float64)) >= 0)
+
+
 def test_log_wide_range():
     x = np.float32(2.0) ** np.linspace(-125, 127, 200001).astype(np.float32)
     got = O.map_f32(O.MAP_LOG, x)

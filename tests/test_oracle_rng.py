@@ -84,6 +84,20 @@ def test_turn_sincos_against_fp64():
     np.testing.assert_array_equal(exact, [[1, 0], [0, 1], [-1, 0], [0, -1]])
 
 
+def test_table_turn_sincos_against_fp64():
+    # the table-driven (cos, sin) of 2 pi m / 2^24 that the sampler uses
+    m = np.concatenate([np.arange(0, 1 << 24, 37, dtype=np.uint32),
+                        (np.arange(256, dtype=np.uint32) << 16),           # table points
+                        (np.arange(256, dtype=np.uint32) << 16) + 0xFFFF])  # bin ends
+    cs = O.turn_sincos_tab(m).astype(np.float64)
+    ang = 2.0 * np.pi * m.astype(np.float64) / 2.0**24
+    assert np.max(np.abs(cs[:, 0] - np.cos(ang))) < 2.0e-7
+    assert np.max(np.abs(cs[:, 1] - np.sin(ang))) < 2.0e-7
+    # at a table point the remainder is 0 and the entry comes back unchanged
+    pts = (np.arange(256, dtype=np.uint32) << 16)
+    np.testing.assert_array_equal(O.turn_sincos_tab(pts), O.turn_sincos(pts))
+
+
 def test_box_muller_against_fp64_formula():
     rng = np.random.default_rng(7)
     xa = rng.integers(0, 2**32, size=200000, dtype=np.uint64).astype(np.uint32)
