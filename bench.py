@@ -86,8 +86,8 @@ def cpu_baseline(w: dict, gens: int) -> dict:
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="rastrigin_proj_cvt_b65536")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-generations", type=int, default=2)
@@ -116,6 +116,7 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         log(f"bench: copied {nbytes} bytes 3 times (counter calibration)")
+        return
     w = W.workload(args.workload)
     n = W.genotype_len(w)
     nb = w["batch"]

@@ -14,7 +14,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liboracle.so")
 
-MAP_LOG, MAP_SINPI, MAP_EXP, MAP_TANH, MAP_SIGMOID = 0, 1, 2, 3, 4
+MAP_LOG, MAP_RSINPI, MAP_EXP, MAP_TANH, MAP_SIGMOID = 0, 1, 2, 3, 4
 
 
 class OrConfig(C.Structure):
@@ -49,7 +49,8 @@ def lib():
             "or_box_muller": (None, [C.c_uint32, C.c_uint32, f32p]),
             "or_logf": (C.c_float, [C.c_float]),
             "or_turn_sincos": (None, [C.c_uint32, f32p]),
-            "or_sinpi": (C.c_float, [C.c_float]),
+            "or_rsinpi": (C.c_float, [C.c_float]),
+            "or_rsin_coef": (None, [C.POINTER(C.c_float)]),
             "or_expf": (C.c_float, [C.c_float]),
             "or_tanhf": (C.c_float, [C.c_float]),
             "or_sigmoidf": (C.c_float, [C.c_float]),
@@ -154,6 +155,12 @@ def map_f32(fn: int, x) -> np.ndarray:
     x = np.ascontiguousarray(np.asarray(x, dtype=np.float32).ravel())
     out = np.zeros_like(x)
     lib().or_map_f32(fn, _ptr(x, C.c_float), _ptr(out, C.c_float), x.size)
+    return out
+
+
+def rsin_coef() -> np.ndarray:
+    out = np.zeros(6, np.float32)
+    lib().or_rsin_coef(_ptr(out, C.c_float))
     return out
 
 

@@ -227,19 +227,36 @@ void or_box_muller(uint32_t xa, uint32_t xb, float out[2]) {
   out[1] = r * cs[1];
 }
 
-/* sin(pi x): reduce to r = x - rint(x) in [-1/2, 1/2] (exact), then the
- * Taylor series of sin(y), y = pi r in [-pi/2, pi/2], to y^13.  The sign of
- * the result may differ from sin(pi x) by (-1)^rint(x); callers square it. */
-float or_sinpi(float x) {
+/* sqrt(20) sin(pi x), up to sign, for the Rastrigin term.  r = x - rint(x)
+ * lies in [-1/2, 1/2] (exact); sqrt(20) sin(pi r) = r P(r^2) with P the
+ * Taylor series in u = r^2 through u^5, whose coefficient k is
+ * sqrt(20) (-1)^k pi^(2k+1) / (2k+1)!, worked out in double and rounded once to
+ * fp32; P is evaluated by Horner's rule from the u^5 end.  The sign may differ
+ * from that of sin(pi x) by (-1)^rint(x); callers square it. */
+static float g_rsin[6];
+static int g_rsin_built = 0;
+
+void or_rsin_coef(float out[6]) {
+  if (!g_rsin_built) {
+    const double pi = 3.14159265358979323846;
+    for (int k = 0; k < 6; ++k) {
+      double c = sqrt(20.0);
+      for (int i = 1; i <= 2 * k + 1; ++i) c *= pi / (double)i;
+      g_rsin[k] = (float)((k & 1) ? -c : c);
+    }
+    g_rsin_built = 1;
+  }
+  for (int k = 0; k < 6; ++k) out[k] = g_rsin[k];
+}
+
+float or_rsinpi(float x) {
+  float c[6];
+  or_rsin_coef(c);
   float r = x - rintf(x);
-  float y = r * kPi;
-  float y2 = y * y;
-  float p = fmaf(y2, 1.0f / 6227020800.0f, -1.0f / 39916800.0f);
-  p = fmaf(y2, p, 1.0f / 362880.0f);
-  p = fmaf(y2, p, -1.0f / 5040.0f);
-  p = fmaf(y2, p, 1.0f / 120.0f);
-  p = fmaf(y2, p, -1.0f / 6.0f);
-  return fmaf(y * y2, p, y);
+  float u = r * r;
+  float q = c[5];
+  for (int k = 4; k >= 0; --k) q = fmaf(u, q, c[k]);
+  return r * q;
 }
 
 /* exp(x): k = rint(x log2 e), r = x - k ln 2 (two steps), Taylor to r^7,
@@ -301,8 +318,9 @@ static float clampf(float x, float lo, float hi) { return fminf(fmaxf(x, lo), hi
 
 /* Rastrigin, Sphere (Appendix B.2) and the two-half projection descriptor.
  * Rastrigin uses 10 - 10 cos(2 pi x) = 20 sin^2(pi x), so that every term
- * x^2 + 20 sin^2(pi x) is non-negative and nothing cancels; the objective is
- * the negated R64 sum of the terms. */
+ * x^2 + 20 sin^2(pi x) = x^2 + s^2 with s = sqrt(20) sin(pi x) is
+ * non-negative and nothing cancels; the objective is the negated R64 sum of
+ * the terms. */
 void or_eval_testfn(int32_t task, const float* x, int32_t n, const float* lo,
                     const float* hi, float* fit, float* desc) {
   float* t = (float*)calloc((size_t)(n > 0 ? n : 1), sizeof(float));
@@ -310,8 +328,8 @@ void or_eval_testfn(int32_t task, const float* x, int32_t n, const float* lo,
     if (task == OR_SPHERE) {
       t[g] = x[g] * x[g];
     } else {
-      float sp = or_sinpi(x[g]);
-      t[g] = fmaf(20.0f, sp * sp, x[g] * x[g]);
+      float sv = or_rsinpi(x[g]);
+      t[g] = fmaf(sv, sv, x[g] * x[g]);
     }
   }
   *fit = -or_r64_sum(t, 0, n);
@@ -777,7 +795,7 @@ void or_map_f32(int32_t fn, const float* in, float* out, int64_t count) {
     float x = in[i];
     switch (fn) {
       case 0: out[i] = or_logf(x); break;
-      case 1: out[i] = or_sinpi(x); break;
+      case 1: out[i] = or_rsinpi(x); break;
       case 2: out[i] = or_expf(x); break;
       case 3: out[i] = or_tanhf(x); break;
       default: out[i] = or_sigmoidf(x); break;

@@ -43,7 +43,8 @@ float    or_u24p(uint32_t x);
 void     or_box_muller(uint32_t xa, uint32_t xb, float out[2]);
 float    or_logf(float x);
 void     or_turn_sincos(uint32_t m24, float out[2]);   /* cos, sin of 2*pi*m/2^24 */
-float    or_sinpi(float x);
+float    or_rsinpi(float x);          /* sqrt(20) sin(pi x), up to sign */
+void     or_rsin_coef(float out[6]);  /* its six polynomial coefficients */
 float    or_expf(float x);
 float    or_tanhf(float x);
 float    or_sigmoidf(float x);

@@ -215,17 +215,27 @@ __device__ __forceinline__ float2 gauss2(uint32_t xa, uint32_t xb, const Tables&
 }
 
 
-// sin(pi x) up to sign: r = x - rint(x) (exact), y = pi r, Taylor to y^13.
-__device__ __forceinline__ float sinpi_unsigned(float x) {
+// sqrt(20) sin(pi x) up to sign (the sign may differ by (-1)^rint(x)):
+// r = x - rint(x) in [-1/2, 1/2] (exact), then r P(r^2), P the Taylor series
+// of sqrt(20) sin(pi r) / r in u = r^2 through u^5 by Horner's rule.  Its
+// coefficient k, sqrt(20) (-1)^k pi^(2k+1) / (2k+1)!, is worked out in double
+// at compile time and rounded once to fp32.
+constexpr float rsin_coef(int k) {
+  double c = 4.47213595499957939282;   // sqrt(20)
+  for (int i = 1; i <= 2 * k + 1; ++i) c *= 3.14159265358979323846 / (double)i;
+  return (float)((k & 1) ? -c : c);
+}
+__device__ __forceinline__ float rsinpi(float x) {
+  constexpr float c0 = rsin_coef(0), c1 = rsin_coef(1), c2 = rsin_coef(2);
+  constexpr float c3 = rsin_coef(3), c4 = rsin_coef(4), c5 = rsin_coef(5);
   const float r = x - __builtin_rintf(x);
-  const float y = r * kPi;
-  const float y2 = y * y;
-  float p = fma32(y2, 1.0f / 6227020800.0f, -1.0f / 39916800.0f);
-  p = fma32(y2, p, 1.0f / 362880.0f);
-  p = fma32(y2, p, -1.0f / 5040.0f);
-  p = fma32(y2, p, 1.0f / 120.0f);
-  p = fma32(y2, p, -1.0f / 6.0f);
-  return fma32(y * y2, p, y);
+  const float u = r * r;
+  float q = fma32(u, c5, c4);
+  q = fma32(u, q, c3);
+  q = fma32(u, q, c2);
+  q = fma32(u, q, c1);
+  q = fma32(u, q, c0);
+  return r * q;
 }
 
 // e^x, input clamped to [-87, 88]: k = rint(x log2 e), r = x - k ln 2 in two
@@ -317,6 +327,30 @@ __device__ __forceinline__ float wave_fold_sum(float v) {
   v = v + row_ror<2>(v);
   v = v + row_ror<1>(v);
   return v;
+}
+
+// The same fold for three values at once.  The first two steps pack values
+// into halves and rows of one register (a half-swap of a with b leaves lane l
+// of the sum holding a_l + a_{l+32} below lane 32 and b's pair sums above;
+// the row swap then does the same for rows of 16 lanes), after which the
+// rotations finish all three in one register: a ends in lanes 0-15, c in
+// 16-31, b in 32-47.  Each value goes through exactly the pairs of
+// wave_fold_sum.
+__device__ __forceinline__ void wave_fold_sum3(float a, float b, float c, float& sa, float& sb,
+                                               float& sc) {
+  const auto ab = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  const float pab = __uint_as_float(ab[0]) + __uint_as_float(ab[1]);
+  const auto cz = __builtin_amdgcn_permlane32_swap(__float_as_uint(c), 0u, false, false);
+  const float pcz = __uint_as_float(cz[0]) + __uint_as_float(cz[1]);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(pab), __float_as_uint(pcz), false, false);
+  float v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  v = v + row_ror<8>(v);
+  v = v + row_ror<4>(v);
+  v = v + row_ror<2>(v);
+  v = v + row_ror<1>(v);
+  sa = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(v), 0));
+  sc = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(v), 16));
+  sb = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(v), 32));
 }
 
 // Order-preserving map of an fp32 objective to u32 (-0 folded onto +0).

@@ -145,8 +145,8 @@ __device__ __forceinline__ float clip(float x, float lo, float hi) {
 template <int TASK>
 __device__ __forceinline__ float task_term(float x) {
   if (TASK == kTaskSphere) return x * x;
-  const float s = sinpi_unsigned(x);
-  return fma32(20.0f, s * s, x * x);
+  const float s = rsinpi(x);   // x^2 + 20 sin^2(pi x) = x^2 + s^2
+  return fma32(s, s, x * x);
 }
 
 // ---------------------------------------------------------------------------
@@ -391,10 +391,11 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
     const int j = j0 + i;
     Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u, tb};
     if (!GEN0) {
-      q.c1 = __shfl(sel.c1, i, 64);
-      q.c2 = __shfl(sel.c2, i, 64);
-      q.banks = (uint32_t)__shfl((int)sel.banks, i, 64);
-      q.lambda = __shfl(sel.lambda, i, 64);
+      // lane i's selection, read into scalar registers (i is wave-uniform)
+      q.c1 = __builtin_amdgcn_readlane(sel.c1, i);
+      q.c2 = __builtin_amdgcn_readlane(sel.c2, i);
+      q.banks = (uint32_t)__builtin_amdgcn_readlane((int)sel.banks, i);
+      q.lambda = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(sel.lambda), i));
       q.row1 = geno_row(p, q.banks & 1u, q.c1);
       q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
     }
@@ -450,24 +451,28 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
         }
       }
     }
-    // every lane gets the folded sums; lane i keeps offspring i's results
-    const float f = -wave_fold_sum(acc);
-    float d0, d1;
+    // folded sums (wave-uniform); lane i keeps offspring i's, and divides the
+    // half sums once after the loop
+    float f, d0, d1;
     if (TASK == kTaskProj) {
-      d0 = wave_fold_sum(dlo) / (float)half;
-      d1 = wave_fold_sum(dhi) / (float)(n - half);
+      wave_fold_sum3(acc, dlo, dhi, f, d0, d1);
     } else {
+      f = wave_fold_sum(acc);
       d0 = clip(__uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g0), 0)), p.lo[0], p.hi[0]);
       d1 = clip(__uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g1), 0)), p.lo[1], p.hi[1]);
     }
     if (lane == i) {
-      my_f = f;
+      my_f = -f;
       my_d0 = d0;
       my_d1 = d1;
     }
   }
   if (mine) {
     const int j = j0 + lane;
+    if (TASK == kTaskProj) {
+      my_d0 = my_d0 / (float)half;
+      my_d1 = my_d1 / (float)(n - half);
+    }
     const float d[2] = {my_d0, my_d1};
     const int cell = my_f == my_f ? (p.tess == kTessGrid ? grid_cell(p, d) : cvt_cell<2>(p, d))
                                   : -1;

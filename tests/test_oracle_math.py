@@ -47,15 +47,40 @@ def test_log_wide_range():
         assert abs(O.map_f32(O.MAP_LOG, [2.0**e])[0] - e * np.log(2.0)) <= 4e-7 * max(1, abs(e))
 
 
-def test_sinpi():
+def test_scaled_sinpi():
+    # sqrt(20) sin(pi x) up to sign, the Rastrigin term's sine
     x = np.linspace(-12, 12, 480001).astype(np.float32)
-    got = np.abs(O.map_f32(O.MAP_SINPI, x).astype(np.float64))
-    ref = np.abs(np.sin(np.pi * x.astype(np.float64)))
-    assert np.max(np.abs(got - ref)) < 2.5e-7
+    got = np.abs(O.map_f32(O.MAP_RSINPI, x).astype(np.float64))
+    ref = np.sqrt(20.0) * np.abs(np.sin(np.pi * x.astype(np.float64)))
+    assert np.max(np.abs(got - ref)) < 1.2e-6
     ints = np.arange(-50, 51, dtype=np.float32)
-    assert np.all(O.map_f32(O.MAP_SINPI, ints) == 0.0)
+    assert np.all(O.map_f32(O.MAP_RSINPI, ints) == 0.0)
     halves = ints + np.float32(0.5)
-    assert np.max(np.abs(np.abs(O.map_f32(O.MAP_SINPI, halves)) - 1.0)) <= 2.0**-23
+    assert np.max(np.abs(np.abs(O.map_f32(O.MAP_RSINPI, halves)) - np.sqrt(20.0))) < 1.2e-6
+    # near 0 the relative error stays within two ulp
+    small = (2.0 ** np.linspace(-30, -2, 2001)).astype(np.float32)
+    exact = np.sqrt(20.0) * np.sin(np.pi * small.astype(np.float64))
+    rel = O.map_f32(O.MAP_RSINPI, small) / exact - 1
+    assert np.max(np.abs(rel)) < 2.0**-22
+
+
+def test_scaled_sinpi_coefficients_are_rounded_taylor_terms():
+    # each coefficient is the fp32 rounding of sqrt(20) (-1)^k pi^(2k+1)/(2k+1)!,
+    # worked out here in 60-digit decimal arithmetic
+    import math
+    from decimal import Decimal, getcontext
+    getcontext().prec = 60
+    pi = Decimal("3.14159265358979323846264338327950288419716939937510582097494459")
+    s20 = Decimal(20).sqrt()
+    got = O.rsin_coef()
+    for k in range(6):
+        exact = s20 * pi ** (2 * k + 1) / math.factorial(2 * k + 1) * (-1) ** k
+        f = np.float32(float(exact))
+        # rounding through double can only differ from direct rounding at a tie
+        lo, hi = np.nextafter(f, np.float32(-np.inf)), np.nextafter(f, np.float32(np.inf))
+        assert abs(Decimal(float(f)) - exact) <= min(abs(Decimal(float(lo)) - exact),
+                                                   abs(Decimal(float(hi)) - exact))
+        assert got[k] == f, (k, got[k], f)
 
 
 def test_exp():
