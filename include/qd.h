@@ -33,7 +33,10 @@
 extern "C" {
 #endif
 
-#define QD_ABI_VERSION 1u
+#define QD_ABI_VERSION 2u
+
+/* Candidate slots per fine bucket of a two-dimensional CVT (see QD_BUF_CAND_*). */
+#define QD_CAND_SLOTS 16
 
 typedef enum {
   QD_OK = 0,
@@ -82,6 +85,11 @@ enum {
   QD_BUF_CENTROIDS,        /* f32 [C][D] CVT centroids                                */
   QD_BUF_BUCKET_START,     /* i32 [num_buckets + 1] CVT bucket offsets                */
   QD_BUF_BUCKET_ITEMS,     /* f32x4 + i32: bucketed centroid copies and indices       */
+  QD_BUF_CAND_COUNT,       /* i32 [cand_buckets] D = 2 CVT: how many centroids can be  */
+                           /*   nearest to some point of each fine bucket             */
+  QD_BUF_CAND_PTS,         /* f32x4 [cand_buckets][QD_CAND_SLOTS] those centroids, in  */
+                           /*   ascending index: (x, y, index bits, 0); a bucket with  */
+                           /*   more than QD_CAND_SLOTS uses the ring search instead   */
   QD_BUF_ENV,              /* f32: A [obs][obs], B [obs][act], s0 [obs]               */
   QD_BUF_OCC_LIST,         /* i32 [C]   filled cells, ascending                       */
   QD_BUF_COUNTERS,         /* i32 [64]  [0] filled cells, [1] flags, [3] internal     */
@@ -105,6 +113,8 @@ typedef struct {
   int32_t row_stride;      /* floats between genotype rows (multiple of 64)          */
   int32_t bucket_res;      /* CVT buckets per dimension (0 for the grid)             */
   int32_t num_buckets;
+  int32_t cand_res;        /* D = 2 CVT with C <= 65536: fine buckets per dimension,  */
+  int32_t cand_buckets;    /*   largest R with R^2 <= 4 C (else both 0)               */
 } qd_layout;
 
 typedef struct {

@@ -317,6 +317,21 @@ template <int N>
 __device__ __forceinline__ float row_ror(float v) {
   return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), 0x120 + N, 0xf, 0xf, false));
 }
+template <int N>
+__device__ __forceinline__ int row_ror(int v) {
+  return (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)v, 0x120 + N, 0xf, 0xf, false);
+}
+
+// One rotation step of a row-wide minimum of (value, index) pairs, smaller
+// index first among equal values.
+template <int N>
+__device__ __forceinline__ void min_pair_row(float& v, int& idx) {
+  const float ov = row_ror<N>(v);
+  const int oi = row_ror<N>(idx);
+  const bool take = ov < v || (ov == v && oi < idx);
+  v = take ? ov : v;
+  idx = take ? oi : idx;
+}
 __device__ __forceinline__ float wave_fold_sum(float v) {
   const auto h32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   v = __uint_as_float(h32[0]) + __uint_as_float(h32[1]);

@@ -23,6 +23,7 @@
 //                 next selection draws from.
 #pragma once
 
+#include "../../include/qd.h"
 #include "qd_device.hpp"
 
 namespace qd {
@@ -48,6 +49,9 @@ struct Params {
   int* bucket_start;              // [num_buckets + 1], then [num_buckets] cursors
   float4* bucket_pts;             // [C]
   int* bucket_idx;                // [C]
+  int cand_res, cand_buckets;     // D = 2 CVT fine buckets (0: none)
+  int* cand_count;                // [cand_buckets]
+  float4* cand_pts;               // [cand_buckets][QD_CAND_SLOTS]
   float* env;
   int* occ_list;
   int* counters;                  // [0] filled cells, [1] flags, [3] occupancy changed
@@ -308,6 +312,48 @@ __device__ int cvt_cell(const Params& p, const float* d) {
   return best_idx;
 }
 
+// Nearest centroid for four offspring at once, on a two-dimensional CVT with
+// candidate lists: the 16 lanes of row i take the descriptor (d0, d1) held by
+// lane i, look up its fine bucket and test one candidate each, then keep the
+// smallest (distance, index) pair of the row -- the brute-force argmin with
+// ties to the lower index, as the list holds every centroid that can win.
+// Lane i gets offspring i's cell: -1 for a NaN descriptor, -2 when its bucket
+// lists more than QD_CAND_SLOTS centroids or the descriptor lies outside the
+// box (the caller then runs the ring search).  Every lane must call it.
+__device__ __forceinline__ int cvt_cell_rows(const Params& p, float d0, float d1, int lane) {
+  const int row = lane >> 4, sub = lane & 15;
+  const float g0 = __shfl(d0, row, 64), g1 = __shfl(d1, row, 64);
+  const bool nan = !(g0 == g0 && g1 == g1);
+  const float u0 = (g0 - p.lo[0]) / p.span[0];
+  const float u1 = (g1 - p.lo[1]) / p.span[1];
+  const bool inside = !nan && u0 >= 0.0f && u0 <= 1.0f && u1 >= 0.0f && u1 <= 1.0f;
+  float best = __builtin_inff();
+  int best_idx = 0x7fffffff;
+  int cnt = 0;
+  if (inside) {
+    const int R = p.cand_res;
+    const int q0 = __builtin_fminf(__builtin_floorf(u0 * (float)R), (float)(R - 1));
+    const int q1 = __builtin_fminf(__builtin_floorf(u1 * (float)R), (float)(R - 1));
+    const int bucket = q0 * R + q1;
+    cnt = p.cand_count[bucket];
+    if (cnt <= QD_CAND_SLOTS && sub < cnt) {
+      const float4 c = p.cand_pts[(size_t)bucket * QD_CAND_SLOTS + sub];
+      const float e0 = u0 - c.x;
+      float acc = fma32(e0, e0, 0.0f);
+      const float e1 = u1 - c.y;
+      acc = fma32(e1, e1, acc);
+      best = acc;
+      best_idx = __float_as_int(c.z);
+    }
+  }
+  min_pair_row<8>(best, best_idx);
+  min_pair_row<4>(best, best_idx);
+  min_pair_row<2>(best, best_idx);
+  min_pair_row<1>(best, best_idx);
+  const int res = nan ? -1 : (inside && cnt <= QD_CAND_SLOTS ? best_idx : -2);
+  return __shfl(res, (lane & 3) * 16, 64);
+}
+
 // Insertion key: order-preserving bits of the objective (-0 as +0), then
 // N_B-1-j so that equal objectives go to the lowest batch index; 0 = none.
 __device__ __forceinline__ uint64_t insert_key(const Params& p, float f, int cell, int j) {
@@ -467,15 +513,19 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
       my_d1 = d1;
     }
   }
+  if (TASK == kTaskProj) {
+    my_d0 = my_d0 / (float)half;
+    my_d1 = my_d1 / (float)(n - half);
+  }
+  const int listed = p.tess == kTessCvt && p.cand_res > 0 ? cvt_cell_rows(p, my_d0, my_d1, lane) : -2;
   if (mine) {
     const int j = j0 + lane;
-    if (TASK == kTaskProj) {
-      my_d0 = my_d0 / (float)half;
-      my_d1 = my_d1 / (float)(n - half);
-    }
     const float d[2] = {my_d0, my_d1};
-    const int cell = my_f == my_f ? (p.tess == kTessGrid ? grid_cell(p, d) : cvt_cell<2>(p, d))
-                                  : -1;
+    int cell = -1;
+    if (my_f == my_f) {
+      if (p.tess == kTessGrid) cell = grid_cell(p, d);
+      else cell = listed != -2 ? listed : cvt_cell<2>(p, d);
+    }
     const uint64_t key = insert_key(p, my_f, cell, j);
     record_offspring(p, j, sel, my_f, d);
     p.off_cell[j] = cell;
@@ -608,14 +658,16 @@ __device__ void compact_filled(const Params& p) {
 }
 
 // ---------------------------------------------------------------------------
-// Winners: a workgroup takes kRegenCells consecutive cells.  For each cell
-// whose key names an offspring, its four waves regenerate that offspring's
-// genotype (256-gene chunks shared out over the waves) into the cell's other
-// bank from the recorded parents.  After a barrier the cells record objective
-// and descriptor, switch to the new bank, and turn the key into the incumbent
-// form (low word all ones: a later offspring must be strictly better).
+// Winners: a workgroup takes kRegenCells consecutive cells, kRegenCellsPerWave
+// to each of its four waves.  For each of its cells whose key names an
+// offspring, a wave regenerates that offspring's genotype into the cell's
+// other bank from the recorded parents; then the wave's cells record
+// objective and descriptor, switch to the new bank, and turn the key into the
+// incumbent form (low word all ones: a later offspring must be strictly
+// better).  No other wave touches those cells.
 // ---------------------------------------------------------------------------
-constexpr int kRegenCells = 8;
+constexpr int kRegenCellsPerWave = 8;
+constexpr int kRegenCells = 4 * kRegenCellsPerWave;
 
 __device__ __forceinline__ void finish_winner(const Params& p, int c, int j, uint64_t key) {
   p.arch_fit[c] = p.off_fit[j];
@@ -629,34 +681,33 @@ __device__ __forceinline__ bool names_offspring(uint64_t key) {
   return key != 0ull && (uint32_t)key != 0xffffffffu;
 }
 
-// Copies the keys of the workgroup's cells first .. first + kRegenCells - 1
-// into LDS (0 past the archive's end) and returns whether any names an
-// offspring of this batch (the same answer in every thread).  Every thread
-// must call it.
+// Copies the keys of the workgroup's cells first .. first + NCELLS - 1 into
+// LDS (0 past the archive's end) and returns whether any names an offspring
+// of this batch (the same answer in every thread).  Every thread must call it.
+template <int NCELLS>
 __device__ __forceinline__ bool stage_keys(const Params& p, int first, uint64_t* s_key) {
-  if (threadIdx.x < kRegenCells) {
+  bool won = false;
+  if (threadIdx.x < NCELLS) {
     const int c = first + (int)threadIdx.x;
-    s_key[threadIdx.x] = c < p.C ? p.arch_key[c] : 0ull;
+    const uint64_t key = c < p.C ? p.arch_key[c] : 0ull;
+    s_key[threadIdx.x] = key;
+    won = names_offspring(key);
   }
-  __syncthreads();
-  bool any = false;
-#pragma unroll
-  for (int t = 0; t < kRegenCells; ++t) any |= names_offspring(s_key[t]);
-  return any;
+  return __syncthreads_or(won) != 0;
 }
 
-// After the genotypes are written: the winners' cells take objective,
-// descriptor, bank and incumbent key.
-__device__ __forceinline__ void finish_cells(const Params& p, int first, const uint64_t* s_key) {
-  __syncthreads();
-  if (threadIdx.x < kRegenCells) {
-    const uint64_t key = s_key[threadIdx.x];
-    if (names_offspring(key)) finish_winner(p, first + (int)threadIdx.x, p.nb - 1 - (int)(uint32_t)key, key);
+// After a wave has written its genotypes: lane t < kRegenCellsPerWave
+// finishes the wave's cell t if it won.
+__device__ __forceinline__ void finish_wave_cells(const Params& p, int wfirst, const uint64_t* w_key,
+                                                  int lane) {
+  if (lane < kRegenCellsPerWave) {
+    const uint64_t key = w_key[lane];
+    if (names_offspring(key)) finish_winner(p, wfirst + lane, p.nb - 1 - (int)(uint32_t)key, key);
   }
 }
 
-// Workgroups 0 .. ceil(C / kRegenCells) - 1 take cells; one more compacts.
-inline unsigned regen_blocks(int C) { return (unsigned)((C + kRegenCells - 1) / kRegenCells) + 1u; }
+// Workgroups 0 .. ceil(C / cells) - 1 take cells; one more compacts.
+inline unsigned regen_blocks(int C, int cells) { return (unsigned)((C + cells - 1) / cells) + 1u; }
 
 template <bool GEN0>
 __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
@@ -668,24 +719,26 @@ __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
   const int first = blockIdx.x * kRegenCells;
   __shared__ uint64_t s_key[kRegenCells];
   __shared__ float2 s_turn[256], s_logt[128];
-  if (!stage_keys(p, first, s_key)) return;
+  if (!stage_keys<kRegenCells>(p, first, s_key)) return;
   if (!GEN0) {
     build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
     __syncthreads();
   }
   const Tables tb{s_turn, s_logt};
-  for (int t = 0; t < kRegenCells; ++t) {
-    const uint64_t key = s_key[t];
+  const int wfirst = first + wave * kRegenCellsPerWave;
+  const uint64_t* w_key = s_key + wave * kRegenCellsPerWave;
+  for (int t = 0; t < kRegenCellsPerWave; ++t) {
+    const uint64_t key = w_key[t];
     if (!names_offspring(key)) continue;
-    const int c = first + t;
+    const int c = wfirst + t;
     const int j = p.nb - 1 - (int)(uint32_t)key;
     Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
     if (!GEN0) q = recorded_pair(p, g, j, tb);
     float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
-    for (int base = 256 * wave + 4 * lane; base < p.n; base += 1024)
+    for (int base = 4 * lane; base < p.n; base += 256)
       *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
   }
-  finish_cells(p, first, s_key);
+  finish_wave_cells(p, wfirst, w_key, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -816,6 +869,42 @@ __global__ void k_bucket_fill(const Params p) {
   const int slot = p.bucket_start[b] + atomicAdd(&cursor[b], 1);
   p.bucket_pts[slot] = make_float4(c[0], c[1], c[2], c[3]);
   p.bucket_idx[slot] = i;
+}
+
+// Candidate lists of a two-dimensional CVT.  Fine bucket (b0, b1) is the box
+// [b0/R, (b0+1)/R] x [b1/R, (b1+1)/R], widened by 1e-6 on every side to cover
+// the rounding of the bucket index.  Every point of it lies within
+// Dmax = min over centroids of the farthest-corner distance of some centroid,
+// so a centroid whose nearest-point distance to the box exceeds Dmax (with a
+// relative margin of 1e-5, far above the fp32 error of the distances the
+// search compares) is never the argmin for a point of the box.  The rest are
+// listed in ascending index; the count keeps counting past QD_CAND_SLOTS.
+__global__ __launch_bounds__(256) void k_cand_build(const Params p) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= p.cand_buckets) return;
+  const int R = p.cand_res;
+  const double w = 1.0 / (double)R, pad = 1e-6;
+  const double lo0 = (b / R) * w - pad, hi0 = (b / R + 1) * w + pad;
+  const double lo1 = (b % R) * w - pad, hi1 = (b % R + 1) * w + pad;
+  double dmax = __builtin_inf();
+  for (int c = 0; c < p.C; ++c) {
+    const double x = p.cent[2 * c], y = p.cent[2 * c + 1];
+    const double fx = fmax(x - lo0, hi0 - x), fy = fmax(y - lo1, hi1 - y);
+    dmax = fmin(dmax, fx * fx + fy * fy);
+  }
+  const double limit = dmax * (1.0 + 1e-5) + 1e-12;
+  int count = 0;
+  float4* out = p.cand_pts + (size_t)b * QD_CAND_SLOTS;
+  for (int c = 0; c < p.C; ++c) {
+    const double x = p.cent[2 * c], y = p.cent[2 * c + 1];
+    const double gx = fmax(0.0, fmax(lo0 - x, x - hi0)), gy = fmax(0.0, fmax(lo1 - y, y - hi1));
+    if (gx * gx + gy * gy <= limit) {
+      if (count < QD_CAND_SLOTS)
+        out[count] = make_float4(p.cent[2 * c], p.cent[2 * c + 1], __int_as_float(c), 0.0f);
+      ++count;
+    }
+  }
+  p.cand_count[b] = count;
 }
 
 // Entry e of [A | B | s0] = 0.1 * normal (e mod 4) of block (e/4, 0, 0, ENV).

@@ -17,6 +17,9 @@ namespace {
 thread_local hipError_t g_last_hip = hipSuccess;
 
 constexpr uint64_t kAlign = 256;
+// Candidate lists are built (one thread per fine bucket, each scanning every
+// centroid twice) only up to this many cells.
+constexpr int kCandMaxCells = 65536;
 
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -94,6 +97,10 @@ qd_status make_layout(const qd_config* c, qd_layout* L) {
     int64_t nbk = 1;
     for (uint64_t k = 0; k < D; ++k) nbk *= L->bucket_res;
     L->num_buckets = (int32_t)nbk;
+    if (c->desc_dim == 2 && c->num_cells <= kCandMaxCells) {
+      L->cand_res = bucket_res_for(4 * c->num_cells, 2);
+      L->cand_buckets = L->cand_res * L->cand_res;
+    }
   }
   const uint64_t env = is_mlp(c) ? (uint64_t)c->mlp_obs * (c->mlp_obs + c->mlp_act + 1) : 0;
   uint64_t bytes[QD_NUM_BUFFERS] = {};
@@ -108,6 +115,8 @@ qd_status make_layout(const qd_config* c, qd_layout* L) {
   bytes[QD_BUF_CENTROIDS] = c->tess == QD_TESS_CVT ? 4 * C * D : 0;
   bytes[QD_BUF_BUCKET_START] = c->tess == QD_TESS_CVT ? 4 * 2 * ((uint64_t)L->num_buckets + 1) : 0;
   bytes[QD_BUF_BUCKET_ITEMS] = c->tess == QD_TESS_CVT ? (16 + 4) * C : 0;
+  bytes[QD_BUF_CAND_COUNT] = 4 * (uint64_t)L->cand_buckets;
+  bytes[QD_BUF_CAND_PTS] = 16 * (uint64_t)QD_CAND_SLOTS * (uint64_t)L->cand_buckets;
   bytes[QD_BUF_ENV] = 4 * env;
   bytes[QD_BUF_OCC_LIST] = 4 * C;
   bytes[QD_BUF_COUNTERS] = 4 * 64;
@@ -228,7 +237,7 @@ template <bool GEN0>
 void launch_regen(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
   Timed t(h, s, QD_K_REGEN);
-  const dim3 grid(qd::regen_blocks(p.C)), block(256);
+  const dim3 grid(qd::regen_blocks(p.C, qd::kRegenCells)), block(256);
   if (p.task == qd::kTaskMlp) qd::launch_mlp_regen(p, GEN0, g, s);
   else hipLaunchKernelGGL((qd::k_regen<GEN0>), grid, block, 0, s, p, g);
 }
@@ -294,6 +303,10 @@ qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
     p.bucket_pts = (float4*)(ws + L->offset[QD_BUF_BUCKET_ITEMS]);
     p.bucket_idx = (int*)(ws + L->offset[QD_BUF_BUCKET_ITEMS] + 16ull * c->num_cells);
   }
+  p.cand_res = L->cand_res;
+  p.cand_buckets = L->cand_buckets;
+  p.cand_count = (int*)at(QD_BUF_CAND_COUNT);
+  p.cand_pts = (float4*)at(QD_BUF_CAND_PTS);
   p.env = (float*)at(QD_BUF_ENV);
   p.occ_list = (int*)at(QD_BUF_OCC_LIST);
   p.counters = (int*)at(QD_BUF_COUNTERS);
@@ -343,6 +356,8 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
       hipLaunchKernelGGL(qd::k_centroids, dim3(blocks_for(p.C, 256)), dim3(256), 0, s, p);
       hipLaunchKernelGGL(qd::k_bucket_scan, dim3(1), dim3(1024), 0, s, p);
       hipLaunchKernelGGL(qd::k_bucket_fill, dim3(blocks_for(p.C, 256)), dim3(256), 0, s, p);
+      if (p.cand_buckets > 0)
+        hipLaunchKernelGGL(qd::k_cand_build, dim3(blocks_for(p.cand_buckets, 256)), dim3(256), 0, s, p);
     }
     if (p.task == qd::kTaskMlp) {
       const int count = p.obs * (p.obs + p.act + 1);

@@ -244,8 +244,14 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   }
 }
 
-// Winners of a policy batch: one wave per cell writes the winning offspring's
-// genotype into the cell's other bank (same gene formula as the prologue).
+// Winners of a policy batch: a workgroup takes kRegenCellsMlp consecutive
+// cells and, for each whose key names an offspring, all 256 threads write
+// that offspring's genotype (same gene formula as the rollout's prologue) into
+// the cell's other bank -- policy rows are long, so one row is spread over the
+// whole workgroup.  After a barrier the cells record objective and descriptor,
+// switch bank and take the incumbent key.
+constexpr int kRegenCellsMlp = 8;
+
 template <bool GEN0>
 __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
   if (blockIdx.x == gridDim.x - 1) {
@@ -253,17 +259,17 @@ __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
     return;
   }
   const int tid = threadIdx.x;
-  const int first = blockIdx.x * kRegenCells;
+  const int first = blockIdx.x * kRegenCellsMlp;
   const int nblk = (p.n + 3) >> 2;
-  __shared__ uint64_t s_key[kRegenCells];
+  __shared__ uint64_t s_key[kRegenCellsMlp];
   __shared__ float2 s_turn[256], s_logt[128];
-  if (!stage_keys(p, first, s_key)) return;
+  if (!stage_keys<kRegenCellsMlp>(p, first, s_key)) return;
   if (!GEN0) {
     build_tables(s_turn, s_logt, tid, 256);
     __syncthreads();
   }
   const Tables tb{s_turn, s_logt};
-  for (int t = 0; t < kRegenCells; ++t) {
+  for (int t = 0; t < kRegenCellsMlp; ++t) {
     const uint64_t key = s_key[t];
     if (!names_offspring(key)) continue;
     const int c = first + t;
@@ -274,7 +280,11 @@ __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
     for (int blk = tid; blk < nblk; blk += 256)
       *reinterpret_cast<float4*>(dst + 4 * blk) = mlp_gene_block<GEN0>(p, q, g, j, blk);
   }
-  finish_cells(p, first, s_key);
+  __syncthreads();
+  if (tid < kRegenCellsMlp) {
+    const uint64_t key = s_key[tid];
+    if (names_offspring(key)) finish_winner(p, first + tid, p.nb - 1 - (int)(uint32_t)key, key);
+  }
 }
 
 inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hipStream_t s) {
@@ -295,7 +305,7 @@ inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hi
 }
 
 inline void launch_mlp_regen(const Params& p, bool gen0, uint32_t g, hipStream_t s) {
-  const dim3 grid(regen_blocks(p.C)), block(256);
+  const dim3 grid(regen_blocks(p.C, kRegenCellsMlp)), block(256);
   if (gen0) hipLaunchKernelGGL((k_regen_mlp<true>), grid, block, 0, s, p, g);
   else hipLaunchKernelGGL((k_regen_mlp<false>), grid, block, 0, s, p, g);
 }

@@ -15,14 +15,15 @@ from . import workloads as W
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqd.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
+CAND_SLOTS = 16
 QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
     QD_ERR_UNSUPPORTED, QD_ERR_HIP = range(6)
 
 (BUF_ARCHIVE_KEY, BUF_ARCHIVE_FIT, BUF_ARCHIVE_DESC, BUF_ARCHIVE_SLOT, BUF_ARCHIVE_GENO,
- BUF_CENTROIDS, BUF_BUCKET_START, BUF_BUCKET_ITEMS, BUF_ENV, BUF_OCC_LIST, BUF_COUNTERS,
- BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC, BUF_OFF_CELL, BUF_OFF_WON, BUF_OFF_KEY,
- BUF_OFF_BANK, BUF_OFF_GENO, BUF_STATS, NUM_BUFFERS) = range(21)
+ BUF_CENTROIDS, BUF_BUCKET_START, BUF_BUCKET_ITEMS, BUF_CAND_COUNT, BUF_CAND_PTS, BUF_ENV,
+ BUF_OCC_LIST, BUF_COUNTERS, BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC, BUF_OFF_CELL,
+ BUF_OFF_WON, BUF_OFF_KEY, BUF_OFF_BANK, BUF_OFF_GENO, BUF_STATS, NUM_BUFFERS) = range(23)
 
 (K_VARY_EVAL, K_ROLLOUT, K_INSERT, K_REGEN, K_SETUP, NUM_KERNELS) = range(6)
 KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
@@ -51,6 +52,7 @@ class QdLayout(C.Structure):
         ("workspace_bytes", C.c_uint64), ("offset", C.c_uint64 * NUM_BUFFERS),
         ("bytes", C.c_uint64 * NUM_BUFFERS), ("genotype_dim", C.c_int32),
         ("row_stride", C.c_int32), ("bucket_res", C.c_int32), ("num_buckets", C.c_int32),
+        ("cand_res", C.c_int32), ("cand_buckets", C.c_int32),
     ]
 
 
@@ -232,6 +234,9 @@ class Archive:
             slot=self.view(BUF_ARCHIVE_SLOT, torch.int32, (C_,)),
             geno=self.view(BUF_ARCHIVE_GENO, torch.float32, (2, C_, st)),
             centroids=self.view(BUF_CENTROIDS, torch.float32, (C_, D)),
+            cand_count=self.view(BUF_CAND_COUNT, torch.int32, (self.layout.cand_buckets,)),
+            cand_pts=self.view(BUF_CAND_PTS, torch.float32,
+                               (self.layout.cand_buckets, CAND_SLOTS, 4)),
             env=self.view(BUF_ENV, torch.float32, (self.layout.bytes[BUF_ENV] // 4,)),
             occ_list=self.view(BUF_OCC_LIST, torch.int32, (C_,)),
             counters=self.view(BUF_COUNTERS, torch.int32, (64,)),

@@ -4,11 +4,48 @@
       kernel trace: kernel, calls, total and average duration
   python -m paper_2202_01258_amd.rocprof_summary --pmc <results.db> [--top N]
       counters (--pmc runs): kernel, counter, dispatches, mean value per dispatch
+  python -m paper_2202_01258_amd.rocprof_summary --traffic KERNEL \
+          <copy_fetch.db> <copy_write.db> <fetch.db> <write.db> --copy-mib M
+      HBM bytes per launch of KERNEL: FETCH_SIZE and WRITE_SIZE (KiB per
+      dispatch) each scaled by bytes moved / counter value of a plain copy of
+      M MiB, with a digest of the kernel sources the counters belong to
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
+import os
 import sqlite3
+
+TRAFFIC_TAG = "traffic_bytes_per_launch"
+
+
+def sources_digest() -> str:
+    """sha256 over the HIP sources and the public header, in name order."""
+    root = os.path.dirname(os.path.abspath(__file__))
+    files = sorted(glob.glob(os.path.join(root, "csrc", "*")))
+    files.append(os.path.join(os.path.dirname(root), "include", "qd.h"))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(summary_path: str, kernel: str) -> float | None:
+    """Bytes per launch recorded for `kernel` in a --traffic summary, or None
+    when the file is absent or was taken on other kernel sources."""
+    if not os.path.exists(summary_path):
+        return None
+    want = sources_digest()
+    with open(summary_path) as fh:
+        for line in fh:
+            parts = line.split(maxsplit=3)
+            if len(parts) == 4 and parts[0] == TRAFFIC_TAG and parts[3].strip() == kernel:
+                return float(parts[1]) if parts[2] == want else None
+    return None
 
 
 def summary(db_path: str, top: int = 20) -> str:
@@ -38,13 +75,47 @@ def pmc_summary(db_path: str, top: int = 20) -> str:
     return "\n".join(out)
 
 
+def _counter_mean(db_path: str, counter: str, name_like: str) -> tuple[float, int]:
+    con = sqlite3.connect(db_path)
+    row = con.execute("select avg(counter_value), count(*) from pmc_events where counter_name = ? "
+                      "and name like ?", (counter, name_like)).fetchone()
+    if row is None or row[1] == 0:
+        raise SystemExit(f"{db_path}: no {counter} rows for kernels like {name_like!r}")
+    return float(row[0]), int(row[1])
+
+
+def traffic(kernel: str, copy_fetch: str, copy_write: str, fetch: str, write: str,
+            copy_mib: int) -> str:
+    copy_bytes = copy_mib * 2.0**20
+    cf, _ = _counter_mean(copy_fetch, "FETCH_SIZE", "%copyBuffer%")
+    cw, _ = _counter_mean(copy_write, "WRITE_SIZE", "%copyBuffer%")
+    f_scale, w_scale = copy_bytes / (cf * 1024.0), copy_bytes / (cw * 1024.0)
+    kf, nf = _counter_mean(fetch, "FETCH_SIZE", f"%{kernel}%")
+    kw, nw = _counter_mean(write, "WRITE_SIZE", f"%{kernel}%")
+    rd, wr = kf * 1024.0 * f_scale, kw * 1024.0 * w_scale
+    return "\n".join([
+        f"copy of {copy_mib} MiB: FETCH_SIZE {cf:.1f} KiB -> scale {f_scale:.4f}; "
+        f"WRITE_SIZE {cw:.1f} KiB -> scale {w_scale:.4f}",
+        f"{kernel}: FETCH_SIZE {kf:.2f} KiB/dispatch ({nf} dispatches) -> {rd:.0f} B read; "
+        f"WRITE_SIZE {kw:.2f} KiB/dispatch ({nw} dispatches) -> {wr:.0f} B written",
+        f"{TRAFFIC_TAG} {rd + wr:.0f} {sources_digest()} {kernel}",
+    ])
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("db")
+    ap.add_argument("db", nargs="+")
     ap.add_argument("--top", type=int, default=20)
     ap.add_argument("--pmc", action="store_true")
+    ap.add_argument("--traffic", metavar="KERNEL")
+    ap.add_argument("--copy-mib", type=int, default=256)
     a = ap.parse_args()
-    print(pmc_summary(a.db, a.top) if a.pmc else summary(a.db, a.top))
+    if a.traffic:
+        if len(a.db) != 4:
+            raise SystemExit("--traffic takes copy_fetch.db copy_write.db fetch.db write.db")
+        print(traffic(a.traffic, *a.db, a.copy_mib))
+    else:
+        print(pmc_summary(a.db[0], a.top) if a.pmc else summary(a.db[0], a.top))
 
 
 if __name__ == "__main__":

@@ -65,6 +65,15 @@ def test_layouts(lib, name):
     assert lay.workspace_bytes >= lay.offset[Q.NUM_BUFFERS - 1] + lay.bytes[Q.NUM_BUFFERS - 1]
     if w["tess"] == W.CVT:
         assert lay.bucket_res ** w["D"] == lay.num_buckets <= w["C"]
+    if w["tess"] == W.CVT and w["D"] == 2:
+        # fine buckets for the candidate lists: largest R with R^2 <= 4 C
+        R = lay.cand_res
+        assert R * R == lay.cand_buckets and R * R <= 4 * w["C"] < (R + 1) * (R + 1)
+        assert lay.bytes[Q.BUF_CAND_COUNT] == 4 * R * R
+        assert lay.bytes[Q.BUF_CAND_PTS] == 16 * Q.CAND_SLOTS * R * R
+    else:
+        assert lay.cand_res == lay.cand_buckets == 0
+        assert lay.bytes[Q.BUF_CAND_COUNT] == lay.bytes[Q.BUF_CAND_PTS] == 0
     keep = Q.layout_query(Q.make_config(w, keep_offspring=True))
     assert keep.bytes[Q.BUF_OFF_GENO] == w["batch"] * lay.row_stride * 4
 

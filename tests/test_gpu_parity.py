@@ -57,12 +57,17 @@ SMALL = {
     "sphere_grid_b16384": dict(batch=1000),
     "rastrigin_proj_cvt_b65536": dict(batch=600),
     "rastrigin_ragged": dict(n=257, batch=77),
+    # projection descriptors spread over the whole box: few genes drawn from the
+    # full range, so the nearest-centroid search meets most fine buckets
+    "proj_spread_cvt": dict(n=8, batch=3000, C=2000, init_lo=-5.12, init_hi=5.12, seed=3),
 }
 
 
 def small_workload(name):
     if name == "rastrigin_ragged":
         return W.workload("rastrigin_grid_b128", n=257, batch=77, seed=5)
+    if name == "proj_spread_cvt":
+        return W.workload("rastrigin_proj_cvt_b65536", **SMALL[name])
     return W.workload(name, **SMALL[name])
 
 
@@ -83,6 +88,51 @@ def test_first_batch_bit_exact(name):
     assert_archive_equal(a.snapshot(), o.archive(), o.n, "after the first batch")
     if w["tess"] == W.CVT:
         np.testing.assert_array_equal(a.views()["centroids"].cpu().numpy(), o.centroids())
+
+
+@pytest.mark.parametrize("C,seed", [(10000, 0), (2000, 3), (37, 1)])
+def test_cvt_candidate_lists_hold_the_nearest_centroid(C, seed):
+    """Every listed fine bucket holds, in ascending order, the brute-force
+    nearest centroid (the oracle's) of points all over it: random points,
+    bucket corners and points one fp32 step either side of bucket edges."""
+    w = W.workload("rastrigin_proj_cvt_b65536", C=C, batch=64, seed=seed)
+    say(f"candidate lists C={C} seed={seed}")
+    a = qd().Archive(w)
+    v = a.views()
+    R = a.layout.cand_res
+    assert R > 0 and R * R <= 4 * C < (R + 1) * (R + 1)
+    cnt = v["cand_count"].cpu().numpy()
+    pts = v["cand_pts"].cpu().numpy()
+    cent = v["centroids"].cpu().numpy()
+    assert cnt.min() >= 1
+    assert (cnt <= qd().CAND_SLOTS).mean() > 0.999
+    o = O.Oracle(w)
+    o.setup()
+    np.testing.assert_array_equal(cent, o.centroids())
+    rng = np.random.default_rng(seed)
+    edges = (np.arange(R + 1) / R).astype(np.float32)
+    near = np.concatenate([edges, np.nextafter(edges, np.float32(0)),
+                           np.nextafter(edges, np.float32(1))]).clip(0, 1)
+    u = np.concatenate([
+        rng.random((4000, 2), dtype=np.float32),
+        np.stack([rng.choice(near, 4000), rng.random(4000, dtype=np.float32)], 1),
+        np.stack([rng.random(4000, dtype=np.float32), rng.choice(near, 4000)], 1),
+        np.stack([rng.choice(near, 2000), rng.choice(near, 2000)], 1),
+    ]).astype(np.float32)
+    lo, hi = np.float32(-5.12), np.float32(5.12)
+    span = np.float32(hi - lo)
+    for k, (u0, u1) in enumerate(u):
+        d = (np.float32(u0) * span + lo, np.float32(u1) * span + lo)
+        d = np.clip(np.array(d, np.float32), lo, hi)
+        best = O.cvt_cell(d, w["lo"], w["hi"], cent)
+        un = (d - lo) / span
+        q = np.minimum(np.floor(un * np.float32(R)), R - 1).astype(int)
+        b = q[0] * R + q[1]
+        if cnt[b] > qd().CAND_SLOTS:
+            continue
+        listed = pts[b, :cnt[b], 2].view(np.int32)
+        assert np.all(np.diff(listed) > 0), (b, listed)
+        assert best in listed, (k, d, b, best, listed)
 
 
 @pytest.mark.parametrize("name", list(SMALL))
