@@ -10,11 +10,12 @@ cells).  Prints one JSON line.
                   [--no-cpu-baseline] [--cpu-generations G]
 
 Throughput `value` = N_B * K / (wall time of the K timed steps), bracketed by
-device synchronisation.  The paper's eval/s (mean over steps of N_B / t_n) is
-reported beside it from per-step HIP events.  The roofline object is for the
-dominant kernel, whose per-launch duration comes from HIP events that the
-library records around each of its launches on its stream, over a second run
-of K steps right after the timed one.
+device synchronisation, with nothing else on the stream.  The paper's eval/s
+(mean over steps of N_B / t_n) and the median step come from a second run of K
+steps with a HIP event after each.  The roofline object is for the dominant
+kernel, whose per-launch duration comes from start/stop HIP events attached to
+each of its launches on its stream (hipExtLaunchKernelGGL) over a third run of
+K steps.
 """
 from __future__ import annotations
 
@@ -132,23 +133,33 @@ def main():
     log(f"bench: {args.warmup} warmup steps done; timing {args.steps} steps")
 
     dominant = "rollout" if w["task"] == 3 else "vary_eval"
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    # full name of the dominant kernel in profiler output, and the committed
+    # HBM-counter summary for it on this workload (see rocprof_summary --traffic)
+    kernel_name = (f"k_rollout<{w['hid']}, false, false>" if w["task"] == 3
+                   else f"k_vary_eval<{w['task']}, false, false>")
+    traffic_file = os.path.join(ROOT, "profiles", f"k_{dominant}_{args.workload}_hbm_traffic.txt")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    for k in range(args.steps):
+        a.generation(g)
+        g += 1
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    wall = t1 - t0
+    # Every event recorded on the stream between two kernels delays the second
+    # by several microseconds, so the timed run above records none.  Per-step
+    # times (for the paper's eval/s) come from a second run of the same number
+    # of steps with an event after each step; the dominant kernel's launch
+    # duration from a third, whose launches carry start/stop events of their
+    # own; every kernel's from a fourth.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     ev[0].record(stream)
     for k in range(args.steps):
         a.generation(g)
         g += 1
         ev[k + 1].record(stream)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    wall = t1 - t0
     step_ms = [ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps)]
-    # The dominant kernel's launch duration: HIP events that the library records
-    # around each of its launches, over a second run of the same number of
-    # steps (events between kernels inside a step lengthen the step by several
-    # microseconds, so they stay out of the run that gives `value`); then
-    # every kernel, in a third run.
     ktimes, breakdown = {}, {}
     if not args.no_kernel_timing:
         a.set_kernel_timing([dominant])
@@ -180,7 +191,7 @@ def main():
                    "batch": nb, "genotype_dim": n, "cells": w["C"],
                    "tessellation": "grid" if w["tess"] == 0 else "cvt",
                    "episode_len": w["T"] if w["task"] == 3 else None, "seed": w["seed"]},
-        "paper_eval_per_s": paper_evals,
+        "paper_eval_per_s": paper_evals,          # second run, per-step events
         "median_step_ms": sorted(step_ms)[len(step_ms) // 2],
         "archive": {"filled_cells": st["num_occupied"], "qd_score": st["qd_score"],
                     "best": st["best"]},
@@ -191,22 +202,26 @@ def main():
         line["kernel_ms_per_step"] = {k: (v[0] / v[1] if v[1] else 0.0)
                                       for k, v in breakdown.items() if v[1]}
     if ktimes:
+        from paper_2202_01258_amd.rocprof_summary import recorded_traffic
+        traffic = recorded_traffic(traffic_file, kernel_name)
         if w["task"] == 3:
             ms, cnt = ktimes["rollout"]
             avg = ms / cnt
             flops = mlp_flops(w) * nb
             ach = flops / (avg * 1e-3) / 1e12
-            line["roofline"] = {"kernel": "k_rollout", "bound": "alu", "achieved": ach,
+            line["roofline"] = {"kernel": kernel_name, "bound": "alu", "achieved": ach,
                                 "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                "frac": ach / FP32_PEAK_TFLOPS, "traffic": None}
+                                "frac": ach / FP32_PEAK_TFLOPS, "traffic": traffic,
+                                "kernel_avg_us": avg * 1e3}
         else:
             ms, cnt = ktimes["vary_eval"]
             avg = ms / cnt
             ach = bytes_model["vary_eval"] * nb / (avg * 1e-3) / 1e9
-            line["roofline"] = {"kernel": "k_vary_eval", "bound": "hbm", "achieved": ach,
+            line["roofline"] = {"kernel": kernel_name, "bound": "hbm", "achieved": ach,
                                 "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                                "frac": ach / HBM_PEAK_GBS, "traffic": None,
-                                "kernel_avg_us": avg * 1e3}
+                                "frac": ach / HBM_PEAK_GBS, "traffic": traffic,
+                                "kernel_avg_us": avg * 1e3,
+                                "algorithmic_bytes_per_launch": bytes_model["vary_eval"] * nb}
     if not args.no_cpu_baseline:
         log("bench: CPU baseline (oracle, one thread)")
         cb_w = dict(w)

@@ -165,9 +165,10 @@ qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_sta
 /* The layout the handle was created with. */
 qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
 
-/* Selects the kernels whose launches are bracketed by HIP events on the launch
- * stream: bit k of kernel_mask is kernel QD_K_k (0 = no timing, the default).
- * QD_ERR_INVALID_ARG for bits beyond QD_NUM_KERNELS. */
+/* Selects the kernels whose launches carry a pair of HIP events on the launch
+ * stream (hipExtLaunchKernelGGL: the runtime stamps them when the dispatch
+ * begins and ends): bit k of kernel_mask is kernel QD_K_k (0 = no timing, the
+ * default).  QD_ERR_INVALID_ARG for bits beyond QD_NUM_KERNELS. */
 qd_status qd_set_kernel_timing(qd_archive* h, uint32_t kernel_mask);
 
 /* Waits for the recorded events and returns, per QD_K_* kernel, the summed

@@ -2,6 +2,7 @@
 // launch sequencing on the caller's stream, per-kernel event timing and error
 // mapping.  The C ABI is declared in include/qd.h.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <cmath>
 #include <cstring>
@@ -172,27 +173,30 @@ hipEvent_t take_event(qd_archive* h) {
   return e;
 }
 
-// Brackets one launch with events when timing is on.
-struct Timed {
+// Launches a kernel on the handle's stream.  When its kernel id is being
+// timed the launch goes through hipExtLaunchKernelGGL with a start/stop event
+// pair, which the runtime stamps when the dispatch begins and ends (no marker
+// packets of their own in the stream).
+struct Go {
   qd_archive* h;
   hipStream_t s;
-  int kernel;
-  hipEvent_t a = nullptr;
-  Timed(qd_archive* h_, hipStream_t s_, int k) : h(h_), s(s_), kernel(k) {
-    if ((h->timing_mask >> kernel) & 1u) {
+  int kernel_id;
+  template <typename K, typename... A>
+  void operator()(K kernel, dim3 grid, dim3 block, A... args) const {
+    hipEvent_t a = nullptr, b = nullptr;
+    if ((h->timing_mask >> kernel_id) & 1u) {
       a = take_event(h);
-      if (a) (void)hipEventRecord(a, s);
-    }
-  }
-  ~Timed() {
-    if (a) {
-      hipEvent_t b = take_event(h);
-      if (b) {
-        (void)hipEventRecord(b, s);
-        h->recs.push_back({kernel, a, b});
-      } else {
+      b = a ? take_event(h) : nullptr;
+      if (a && !b) {
         h->pool.push_back(a);
+        a = nullptr;
       }
+    }
+    if (a) {
+      hipExtLaunchKernelGGL(kernel, grid, block, 0, s, a, b, 0u, args...);
+      h->recs.push_back({kernel_id, a, b});
+    } else {
+      hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
     }
   }
 };
@@ -205,12 +209,12 @@ template <bool GEN0>
 void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
   const dim3 grid(blocks_for((uint64_t)p.nb, 4 * qd::kOffspringPerWave)), block(256);
-  Timed t(h, s, QD_K_VARY_EVAL);
+  const Go go{h, s, QD_K_VARY_EVAL};
   const bool keep = h->cfg.keep_offspring != 0;
-#define QD_VE(TASK)                                                                      \
-  do {                                                                                   \
-    if (keep) hipLaunchKernelGGL((qd::k_vary_eval<TASK, GEN0, true>), grid, block, 0, s, p, g); \
-    else hipLaunchKernelGGL((qd::k_vary_eval<TASK, GEN0, false>), grid, block, 0, s, p, g);     \
+#define QD_VE(TASK)                                                            \
+  do {                                                                         \
+    if (keep) go(qd::k_vary_eval<TASK, GEN0, true>, grid, block, p, g);        \
+    else go(qd::k_vary_eval<TASK, GEN0, false>, grid, block, p, g);           \
   } while (0)
   switch (p.task) {
     case qd::kTaskRastrigin: QD_VE(qd::kTaskRastrigin); break;
@@ -222,33 +226,33 @@ void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
 
 void launch_insert(qd_archive* h, hipStream_t s) {
   const qd::Params& p = h->p;
-  Timed t(h, s, QD_K_INSERT);
+  const Go go{h, s, QD_K_INSERT};
   const dim3 grid(blocks_for((uint64_t)p.nb, qd::kInsertBlock)), block(qd::kInsertBlock);
   if (p.tess == qd::kTessGrid) {
-    if (p.D == 2) hipLaunchKernelGGL((qd::k_insert<qd::kTessGrid, 2>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((qd::k_insert<qd::kTessGrid, 4>), grid, block, 0, s, p);
+    if (p.D == 2) go(qd::k_insert<qd::kTessGrid, 2>, grid, block, p);
+    else go(qd::k_insert<qd::kTessGrid, 4>, grid, block, p);
   } else {
-    if (p.D == 2) hipLaunchKernelGGL((qd::k_insert<qd::kTessCvt, 2>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((qd::k_insert<qd::kTessCvt, 4>), grid, block, 0, s, p);
+    if (p.D == 2) go(qd::k_insert<qd::kTessCvt, 2>, grid, block, p);
+    else go(qd::k_insert<qd::kTessCvt, 4>, grid, block, p);
   }
 }
 
 template <bool GEN0>
 void launch_regen(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
-  Timed t(h, s, QD_K_REGEN);
-  const dim3 grid(qd::regen_blocks(p.C, qd::kRegenCells)), block(256);
-  if (p.task == qd::kTaskMlp) qd::launch_mlp_regen(p, GEN0, g, s);
-  else hipLaunchKernelGGL((qd::k_regen<GEN0>), grid, block, 0, s, p, g);
+  const Go go{h, s, QD_K_REGEN};
+  if (p.task == qd::kTaskMlp) {
+    qd::launch_mlp_regen(p, GEN0, g, go);
+  } else {
+    const dim3 grid(qd::regen_blocks(p.C, qd::kRegenCells)), block(256);
+    go(qd::k_regen<GEN0>, grid, block, p, g);
+  }
 }
 
 template <bool GEN0>
 qd_status enqueue_generation(qd_archive* h, hipStream_t s, uint32_t g) {
   if (h->p.task == qd::kTaskMlp) {
-    {
-      Timed t(h, s, QD_K_ROLLOUT);
-      qd::launch_rollout(h->p, GEN0, g, h->cfg.keep_offspring != 0, s);
-    }
+    qd::launch_rollout(h->p, GEN0, g, h->cfg.keep_offspring != 0, Go{h, s, QD_K_ROLLOUT});
     launch_insert(h, s);
   } else {
     launch_vary_eval<GEN0>(h, s, g);   // also finds cells and inserts
@@ -350,19 +354,17 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
   hipStream_t s = (hipStream_t)stream;
   const qd::Params& p = h->p;
   {
-    Timed t(h, s, QD_K_SETUP);
-    hipLaunchKernelGGL(qd::k_clear_archive, dim3(1024), dim3(256), 0, s, p, 1);
+    const Go go{h, s, QD_K_SETUP};
+    go(qd::k_clear_archive, dim3(1024), dim3(256), p, 1);
     if (p.tess == qd::kTessCvt) {
-      hipLaunchKernelGGL(qd::k_centroids, dim3(blocks_for(p.C, 256)), dim3(256), 0, s, p);
-      hipLaunchKernelGGL(qd::k_bucket_scan, dim3(1), dim3(1024), 0, s, p);
-      hipLaunchKernelGGL(qd::k_bucket_fill, dim3(blocks_for(p.C, 256)), dim3(256), 0, s, p);
-      if (p.cand_buckets > 0)
-        hipLaunchKernelGGL(qd::k_cand_build, dim3(blocks_for(p.cand_buckets, 256)), dim3(256), 0, s, p);
+      go(qd::k_centroids, dim3(blocks_for(p.C, 256)), dim3(256), p);
+      go(qd::k_bucket_scan, dim3(1), dim3(1024), p);
+      go(qd::k_bucket_fill, dim3(blocks_for(p.C, 256)), dim3(256), p);
+      if (p.cand_buckets > 0) go(qd::k_cand_build, dim3(blocks_for(p.cand_buckets, 256)), dim3(256), p);
     }
     if (p.task == qd::kTaskMlp) {
       const int count = p.obs * (p.obs + p.act + 1);
-      hipLaunchKernelGGL(qd::k_env, dim3(blocks_for((count + 3) / 4, 256)), dim3(256), 0, s, p,
-                         count);
+      go(qd::k_env, dim3(blocks_for((count + 3) / 4, 256)), dim3(256), p, count);
     }
   }
   st = enqueue_generation<true>(h, s, 0u);

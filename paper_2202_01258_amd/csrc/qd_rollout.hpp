@@ -287,27 +287,30 @@ __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
   }
 }
 
-inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, hipStream_t s) {
+// Launchers: `go(kernel, grid, block, args...)` makes the launch.
+template <class Go>
+inline void launch_rollout(const Params& p, bool gen0, uint32_t g, bool keep, const Go& go) {
   const dim3 grid((unsigned)p.nb);
-#define QD_RO(H)                                                                                \
-  do {                                                                                          \
-    if (gen0) {                                                                                 \
-      if (keep) hipLaunchKernelGGL((k_rollout<H, true, true>), grid, dim3(H), 0, s, p, g);      \
-      else hipLaunchKernelGGL((k_rollout<H, true, false>), grid, dim3(H), 0, s, p, g);          \
-    } else {                                                                                    \
-      if (keep) hipLaunchKernelGGL((k_rollout<H, false, true>), grid, dim3(H), 0, s, p, g);     \
-      else hipLaunchKernelGGL((k_rollout<H, false, false>), grid, dim3(H), 0, s, p, g);         \
-    }                                                                                           \
+#define QD_RO(H)                                                        \
+  do {                                                                  \
+    if (gen0) {                                                         \
+      if (keep) go(k_rollout<H, true, true>, grid, dim3(H), p, g);      \
+      else go(k_rollout<H, true, false>, grid, dim3(H), p, g);          \
+    } else {                                                            \
+      if (keep) go(k_rollout<H, false, true>, grid, dim3(H), p, g);     \
+      else go(k_rollout<H, false, false>, grid, dim3(H), p, g);         \
+    }                                                                   \
   } while (0)
   if (p.hid == 64) QD_RO(64);
   else QD_RO(128);
 #undef QD_RO
 }
 
-inline void launch_mlp_regen(const Params& p, bool gen0, uint32_t g, hipStream_t s) {
+template <class Go>
+inline void launch_mlp_regen(const Params& p, bool gen0, uint32_t g, const Go& go) {
   const dim3 grid(regen_blocks(p.C, kRegenCellsMlp)), block(256);
-  if (gen0) hipLaunchKernelGGL((k_regen_mlp<true>), grid, block, 0, s, p, g);
-  else hipLaunchKernelGGL((k_regen_mlp<false>), grid, block, 0, s, p, g);
+  if (gen0) go(k_regen_mlp<true>, grid, block, p, g);
+  else go(k_regen_mlp<false>, grid, block, p, g);
 }
 
 }  // namespace qd

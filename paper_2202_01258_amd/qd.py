@@ -175,6 +175,7 @@ class Archive:
                                          C.c_void_p(_stream_handle(self.stream)), C.byref(h)),
                    "qd_archive_init")
         self._h = h
+        self._destroy = lib().qd_archive_destroy
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -183,7 +184,7 @@ class Archive:
                 self.stream.synchronize()
             except Exception:
                 pass
-            lib().qd_archive_destroy(h)
+            self._destroy(h)   # bound at creation: module globals may be gone at exit
             self._h = None
 
     # -- the path
