@@ -205,12 +205,14 @@ def test_replay_is_deterministic():
         np.testing.assert_array_equal(a.snapshot()[k], b.snapshot()[k])
 
 
-def test_full_size_rastrigin_projection_sampled():
-    """N_B = 65536, n = 1000, CVT 10^4: the benchmark's launch configuration.
-    Every offspring's cell and the whole insertion are checked (driven), and
-    sampled offspring genotypes/objectives/descriptors from the oracle."""
-    w = W.workload("rastrigin_proj_cvt_b65536")
-    say("full size rastrigin projection: init")
+@pytest.mark.parametrize("batch", [65536, 131072])
+def test_full_size_rastrigin_projection_sampled(batch):
+    """n = 1000, CVT 10^4 at N_B = 65536 (the benchmark's launch configuration)
+    and at 131072 (the top of the batch-size sweep).  Every offspring's cell
+    and the whole insertion are checked (driven), and sampled offspring
+    genotypes/objectives/descriptors from the oracle."""
+    w = W.workload("rastrigin_proj_cvt_b65536", batch=batch)
+    say(f"full size rastrigin projection N_B={batch}: init")
     a = qd().Archive(w)
     o = O.Oracle(w)
     o.setup()
@@ -277,12 +279,15 @@ def test_mlp_bit_exact(name):
     assert a.stats()["qd_score"] == pytest.approx(o.stats()["qd_score"], rel=1e-12)
 
 
-@pytest.mark.parametrize("name,samples", [("mlp64_cvt_b8192", 6), ("mlp128_cvt_b65536", 2)])
-def test_mlp_full_size_sampled(name, samples):
-    """The full policy shapes (N_B 8192 / 65536, T 250 / 1000): sampled
-    offspring rollouts against the oracle, all cells and insertion driven."""
-    w = W.workload(name)
-    say(f"mlp full size {name}: init")
+@pytest.mark.parametrize("name,batch,samples", [("mlp64_cvt_b8192", 8192, 6),
+                                                ("mlp64_cvt_b8192", 131072, 4),
+                                                ("mlp128_cvt_b65536", 65536, 2)])
+def test_mlp_full_size_sampled(name, batch, samples):
+    """The full policy shapes (N_B 8192 / 65536, T 250 / 1000) and the h = 64
+    shape at the top of the batch-size sweep: sampled offspring rollouts
+    against the oracle, all cells and insertion driven."""
+    w = W.workload(name, batch=batch)
+    say(f"mlp full size {name} N_B={batch}: init")
     a = qd().Archive(w)
     o = O.Oracle(w)
     o.setup()
