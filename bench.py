@@ -93,6 +93,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-generations", type=int, default=2)
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--cvt-lloyd", type=int, nargs=2, metavar=("SAMPLES", "ITERS"),
+                    help="build the CVT with Lloyd iterations over uniform points instead of "
+                         "keeping the uniform centroids")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run 3 plain device-to-device copies of MIB MiB (the reference "
                          "kernel for scaling HBM byte counters) and exit after them")
@@ -119,12 +122,17 @@ def main():
         log(f"bench: copied {nbytes} bytes 3 times (counter calibration)")
         return
     w = W.workload(args.workload)
+    if args.cvt_lloyd:
+        w.update(cvt_samples=args.cvt_lloyd[0], cvt_iters=args.cvt_lloyd[1])
     n = W.genotype_len(w)
     nb = w["batch"]
     log(f"bench: workload {args.workload} N_B={nb} n={n} C={w['C']}; setting up")
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
     a = qd.Archive(w, device="cuda:0")
     stream = a.stream
     stream.synchronize()
+    setup_s = time.perf_counter() - ts
     g = 1
     for _ in range(args.warmup):
         a.generation(g)
@@ -190,7 +198,9 @@ def main():
                    "rastrigin_projection", "mlp_policy"][w["task"]],
                    "batch": nb, "genotype_dim": n, "cells": w["C"],
                    "tessellation": "grid" if w["tess"] == 0 else "cvt",
-                   "episode_len": w["T"] if w["task"] == 3 else None, "seed": w["seed"]},
+                   "episode_len": w["T"] if w["task"] == 3 else None, "seed": w["seed"],
+                   "cvt_lloyd": [w["cvt_samples"], w["cvt_iters"]] if w["cvt_iters"] else None},
+        "setup_s": setup_s,                       # archive set-up and the first batch
         "paper_eval_per_s": paper_evals,          # second run, per-step events
         "median_step_ms": sorted(step_ms)[len(step_ms) // 2],
         "archive": {"filled_cells": st["num_occupied"], "qd_score": st["qd_score"],

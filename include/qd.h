@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define QD_ABI_VERSION 2u
+#define QD_ABI_VERSION 3u
 
 /* Candidate slots per fine bucket of a two-dimensional CVT (see QD_BUF_CAND_*). */
 #define QD_CAND_SLOTS 16
@@ -72,6 +72,10 @@ typedef struct {
   int32_t mlp_act;        /*         actions (8)                                  */
   int32_t episode_len;    /*         rollout steps T                              */
   int32_t keep_offspring; /* 1: also store every offspring genotype (tests)       */
+  int32_t cvt_samples;    /* CVT: Lloyd iterations over this many uniform points  */
+  int32_t cvt_iters;      /*   at set-up (0, 0: centroids stay uniform draws);    */
+                          /*   0 <= cvt_samples <= 2^28, 0 <= cvt_iters <= 10^4,  */
+                          /*   both 0 for the grid                                */
   uint64_t seed;          /* key of every Philox4x32-10 stream                    */
 } qd_config;
 
@@ -90,6 +94,7 @@ enum {
   QD_BUF_CAND_PTS,         /* f32x4 [cand_buckets][QD_CAND_SLOTS] those centroids, in  */
                            /*   ascending index: (x, y, index bits, 0); a bucket with  */
                            /*   more than QD_CAND_SLOTS uses the ring search instead   */
+  QD_BUF_LLOYD_ACC,        /* u64 [C][D + 1] Lloyd point sums and counts (set-up)     */
   QD_BUF_ENV,              /* f32: A [obs][obs], B [obs][act], s0 [obs]               */
   QD_BUF_OCC_LIST,         /* i32 [C]   filled cells, ascending                       */
   QD_BUF_COUNTERS,         /* i32 [64]  [0] filled cells, [1] flags, [3] internal     */
@@ -140,9 +145,11 @@ enum { QD_K_VARY_EVAL = 0, QD_K_ROLLOUT, QD_K_INSERT, QD_K_REGEN, QD_K_SETUP,
 qd_status qd_layout_query(const qd_config* cfg, qd_layout* out);
 
 /* Creates an archive in the caller's workspace and enqueues its first
- * iteration on `stream` (Algorithm 1, random solutions): CVT centroids and the
- * synthetic environment from their Philox streams, an empty archive, N_B
- * random genotypes evaluated and inserted.  Asynchronous: returns once the
+ * iteration on `stream` (Algorithm 1, random solutions): CVT centroids (uniform
+ * draws, then cvt_iters Lloyd iterations over cvt_samples uniform points: each
+ * point to its nearest centroid, each centroid that received points to their
+ * mean) and the synthetic environment from their Philox streams, an empty
+ * archive, N_B random genotypes evaluated and inserted.  Asynchronous: returns once the
  * work is enqueued.  *out receives a host handle owned by the library (free it
  * with qd_archive_destroy).  The workspace must stay valid until then. */
 qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t workspace_bytes,

@@ -25,7 +25,7 @@ class OrConfig(C.Structure):
         ("iso_sigma", C.c_float), ("line_sigma", C.c_float),
         ("init_lo", C.c_float), ("init_hi", C.c_float),
         ("obs", C.c_int32), ("hid", C.c_int32), ("act", C.c_int32), ("T", C.c_int32),
-        ("seed", C.c_uint64),
+        ("cvt_samples", C.c_int32), ("cvt_iters", C.c_int32), ("seed", C.c_uint64),
     ]
 
 
@@ -107,6 +107,7 @@ def make_config(w: dict) -> OrConfig:
     c.iso_sigma, c.line_sigma = w["iso_sigma"], w["line_sigma"]
     c.init_lo, c.init_hi = w["init_lo"], w["init_hi"]
     c.obs, c.hid, c.act, c.T = w["obs"], w["hid"], w["act"], w["T"]
+    c.cvt_samples, c.cvt_iters = w.get("cvt_samples", 0), w.get("cvt_iters", 0)
     c.seed = w["seed"]
     return c
 

@@ -71,7 +71,8 @@ void or_philox(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
 }
 
 /* Stream tags (fourth counter word).  Counter = (item, individual, generation, tag). */
-enum { TAG_INIT = 0, TAG_SELECT = 1, TAG_ISO = 2, TAG_CENTROID = 3, TAG_ENV = 4 };
+enum { TAG_INIT = 0, TAG_SELECT = 1, TAG_ISO = 2, TAG_CENTROID = 3, TAG_ENV = 4,
+       TAG_CVT_SAMPLE = 5 };
 
 static void draw(const or_state* s, uint32_t item, uint32_t indiv, uint32_t gen,
                  uint32_t tag, uint32_t out[4]);
@@ -368,6 +369,8 @@ int32_t or_grid_cell(const float* d, int32_t D, const int32_t* grid, const float
   return cell;
 }
 
+static int32_t nearest_centroid(const float* u, int32_t D, const float* cent, int32_t C);
+
 int32_t or_cvt_cell(const float* d, int32_t D, const float* lo, const float* hi,
                     const float* cent, int32_t C) {
   float u[4];
@@ -375,6 +378,12 @@ int32_t or_cvt_cell(const float* d, int32_t D, const float* lo, const float* hi,
     if (!(d[k] == d[k])) return -1;
     u[k] = (d[k] - lo[k]) / (hi[k] - lo[k]);
   }
+  return nearest_centroid(u, D, cent, C);
+}
+
+/* Brute-force nearest centroid of a point u of [0,1]^D: squared distance as
+ * an fma chain over the dimensions from 0, first minimum in index order. */
+static int32_t nearest_centroid(const float* u, int32_t D, const float* cent, int32_t C) {
   int32_t best = -1;
   float bestd = 0.0f;
   for (int32_t c = 0; c < C; ++c) {
@@ -560,6 +569,42 @@ void or_free(or_state* s) {
  * block (c, 0, 0, CENTROID).  Environment: entry e of [A | B | s0] is 0.1
  * times normal number e mod 4 of block (e/4, 0, 0, ENV), the block's words
  * giving two Box-Muller pairs. */
+/* Centroidal Voronoi tessellation by Lloyd's algorithm (the CVT the paper
+ * cites for its tessellations): cvt_iters times, every one of cvt_samples
+ * uniform points of [0,1]^D (point i, coordinate k = U24 of word k of block
+ * (i, 0, 0, CVT_SAMPLE)) goes to its nearest centroid, and every centroid
+ * that received points moves to their mean; the others stay.  A point's
+ * coordinate is m 2^-24 with an integer m < 2^24, so a centroid's coordinate
+ * sum is kept exactly as the sum of the m; the new coordinate is
+ * ((double)sum / (double)count) 2^-24 rounded to fp32. */
+static void lloyd(or_state* s) {
+  const or_config* c = &s->cfg;
+  const int32_t C = c->C, D = c->D;
+  uint64_t* sum = (uint64_t*)calloc((size_t)C * D, sizeof(uint64_t));
+  uint64_t* cnt = (uint64_t*)calloc((size_t)C, sizeof(uint64_t));
+  for (int32_t it = 0; it < c->cvt_iters; ++it) {
+    memset(sum, 0, (size_t)C * D * sizeof(uint64_t));
+    memset(cnt, 0, (size_t)C * sizeof(uint64_t));
+    for (int32_t i = 0; i < c->cvt_samples; ++i) {
+      uint32_t x[4];
+      float u[4];
+      draw(s, (uint32_t)i, 0, 0, TAG_CVT_SAMPLE, x);
+      for (int32_t k = 0; k < D; ++k) u[k] = or_u24(x[k]);
+      const int32_t b = nearest_centroid(u, D, s->cent, C);
+      for (int32_t k = 0; k < D; ++k) sum[(size_t)b * D + k] += x[k] >> 8;
+      cnt[b] += 1;
+    }
+    for (int32_t b = 0; b < C; ++b) {
+      if (cnt[b] == 0) continue;
+      for (int32_t k = 0; k < D; ++k)
+        s->cent[(size_t)b * D + k] =
+            (float)(((double)sum[(size_t)b * D + k] / (double)cnt[b]) * 0x1p-24);
+    }
+  }
+  free(sum);
+  free(cnt);
+}
+
 void or_setup(or_state* s) {
   const or_config* c = &s->cfg;
   if (c->tess == OR_CVT) {
@@ -568,6 +613,7 @@ void or_setup(or_state* s) {
       draw(s, (uint32_t)i, 0, 0, TAG_CENTROID, x);
       for (int32_t k = 0; k < c->D; ++k) s->cent[(size_t)i * c->D + k] = or_u24(x[k]);
     }
+    if (c->cvt_samples > 0) lloyd(s);
   }
   int32_t ne = or_env_len(c);
   for (int32_t e = 0; e < ne; ++e) {

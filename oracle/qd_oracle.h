@@ -31,6 +31,8 @@ typedef struct {
   float iso_sigma, line_sigma;
   float init_lo, init_hi;
   int32_t obs, hid, act, T;   /* MLP policy and rollout                         */
+  int32_t cvt_samples;  /* CVT: Lloyd iterations over this many uniform points  */
+  int32_t cvt_iters;    /*      (0 = centroids stay the uniform draws)          */
   uint64_t seed;
 } or_config;
 

@@ -18,7 +18,8 @@ namespace qd {
 // Philox4x32 with 10 rounds (Salmon et al., SC'11).  Counter words:
 // (item, individual, generation, stream tag); key = the 64-bit seed.
 // ---------------------------------------------------------------------------
-enum : uint32_t { kTagInit = 0, kTagSelect = 1, kTagIso = 2, kTagCentroid = 3, kTagEnv = 4 };
+enum : uint32_t { kTagInit = 0, kTagSelect = 1, kTagIso = 2, kTagCentroid = 3, kTagEnv = 4,
+                  kTagCvtSample = 5 };
 
 struct Key {
   uint32_t k0, k1;

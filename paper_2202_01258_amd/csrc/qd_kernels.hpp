@@ -49,6 +49,8 @@ struct Params {
   int* bucket_start;              // [num_buckets + 1], then [num_buckets] cursors
   float4* bucket_pts;             // [C]
   int* bucket_idx;                // [C]
+  int cvt_samples;                // Lloyd points (set-up only)
+  unsigned long long* lloyd_acc;  // [C][D + 1]: coordinate numerator sums, count
   int cand_res, cand_buckets;     // D = 2 CVT fine buckets (0: none)
   int* cand_count;                // [cand_buckets]
   float4* cand_pts;               // [cand_buckets][QD_CAND_SLOTS]
@@ -805,6 +807,8 @@ __global__ void k_clear_archive(const Params p, int clear_geno) {
     for (size_t i = tid; i < nv; i += nthr) gp[i] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
   if (tid < 64) p.counters[tid] = 0;
+  if (p.lloyd_acc)
+    for (size_t b = tid; b < (size_t)p.C * (p.D + 1); b += nthr) p.lloyd_acc[b] = 0ull;
   if (p.num_buckets > 0)
     for (size_t b = tid; b < (size_t)2 * (p.num_buckets + 1); b += nthr) p.bucket_start[b] = 0;
 }
@@ -826,7 +830,91 @@ __global__ void k_centroids(const Params p) {
   const uint4 x = philox((uint32_t)i, 0u, 0u, kTagCentroid, p.key);
   const float c[4] = {unit24(x.x), unit24(x.y), unit24(x.z), unit24(x.w)};
   for (int k = 0; k < p.D; ++k) p.cent[(size_t)i * p.D + k] = c[k];
+}
+
+// Centroids per bucket of the ring-search grid (counts at [1 .. num_buckets]).
+__global__ void k_bucket_count(const Params p) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= p.C) return;
+  float c[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < p.D; ++k) c[k] = p.cent[(size_t)i * p.D + k];
   atomicAdd(&p.bucket_start[centroid_bucket(p, c) + 1], 1);
+}
+
+// Lloyd's algorithm for a centroidal Voronoi tessellation, one iteration in
+// two kernels.  Assignment: point i (coordinate k = U24 of word k of block
+// (i, 0, 0, CVT_SAMPLE)) goes to its nearest centroid by the cell rule (fma
+// chain over the dimensions, first minimum in index order); the centroids
+// pass through LDS in tiles of kLloydTile, in index order.  Each point adds
+// its coordinates' 24-bit numerators and a count to its centroid's
+// accumulators -- integer sums, so the order of the atomics does not matter.
+constexpr int kLloydBlock = 256;
+constexpr int kLloydTile = 1024;
+
+template <int D>
+__global__ __launch_bounds__(kLloydBlock) void k_lloyd_assign(const Params p) {
+  __shared__ float4 s_c[kLloydTile];
+  const int i = blockIdx.x * kLloydBlock + threadIdx.x;
+  const bool live = i < p.cvt_samples;
+  const uint4 x = philox((uint32_t)i, 0u, 0u, kTagCvtSample, p.key);
+  const uint32_t m[4] = {x.x >> 8, x.y >> 8, x.z >> 8, x.w >> 8};
+  float u[D];
+#pragma unroll
+  for (int k = 0; k < D; ++k) u[k] = (float)m[k] * 0x1p-24f;
+  float best = __builtin_inff();
+  int best_idx = 0;
+  for (int t0 = 0; t0 < p.C; t0 += kLloydTile) {
+    const int n = p.C - t0 < kLloydTile ? p.C - t0 : kLloydTile;
+    __syncthreads();
+    for (int t = threadIdx.x; t < n; t += kLloydBlock) {
+      const float* c = p.cent + (size_t)(t0 + t) * D;
+      float4 v = make_float4(c[0], c[1], 0.0f, 0.0f);
+      if (D == 4) {
+        v.z = c[2];
+        v.w = c[3];
+      }
+      s_c[t] = v;
+    }
+    __syncthreads();
+    for (int t = 0; t < n; ++t) {
+      const float4 c = s_c[t];
+      const float e0 = u[0] - c.x;
+      float acc = fma32(e0, e0, 0.0f);
+      const float e1 = u[1] - c.y;
+      acc = fma32(e1, e1, acc);
+      if (D == 4) {
+        const float e2 = u[D > 2 ? 2 : 0] - c.z;
+        acc = fma32(e2, e2, acc);
+        const float e3 = u[D > 3 ? 3 : 0] - c.w;
+        acc = fma32(e3, e3, acc);
+      }
+      if (acc < best) {
+        best = acc;
+        best_idx = t0 + t;
+      }
+    }
+  }
+  if (live) {
+    unsigned long long* a = p.lloyd_acc + (size_t)best_idx * (D + 1);
+#pragma unroll
+    for (int k = 0; k < D; ++k) atomicAdd(a + k, (unsigned long long)m[k]);
+    atomicAdd(a + D, 1ull);
+  }
+}
+
+// Update: a centroid that received points moves to their mean,
+// ((double)sum / (double)count) 2^-24 rounded to fp32; the accumulators are
+// cleared for the next iteration.
+__global__ void k_lloyd_update(const Params p) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= p.C) return;
+  unsigned long long* a = p.lloyd_acc + (size_t)c * (p.D + 1);
+  const unsigned long long cnt = a[p.D];
+  if (cnt != 0ull) {
+    for (int k = 0; k < p.D; ++k)
+      p.cent[(size_t)c * p.D + k] = (float)(((double)a[k] / (double)cnt) * 0x1p-24);
+  }
+  for (int k = 0; k <= p.D; ++k) a[k] = 0ull;
 }
 
 __global__ __launch_bounds__(1024) void k_bucket_scan(const Params p) {

@@ -55,6 +55,11 @@ qd_status validate(const qd_config* c) {
   if (c->batch_size < 1) return QD_ERR_INVALID_ARG;
   if (c->num_cells < 1 || c->num_cells > (1 << 28)) return QD_ERR_INVALID_ARG;
   if (c->keep_offspring != 0 && c->keep_offspring != 1) return QD_ERR_INVALID_ARG;
+  if (c->cvt_samples < 0 || c->cvt_samples > (1 << 28) || c->cvt_iters < 0 ||
+      c->cvt_iters > 10000)
+    return QD_ERR_INVALID_ARG;
+  if (c->tess == QD_TESS_GRID && (c->cvt_samples != 0 || c->cvt_iters != 0))
+    return QD_ERR_INVALID_ARG;
   const int D = c->desc_dim;
   if (is_mlp(c)) {
     if (c->genotype_dim != 0 || D != 4) return QD_ERR_INVALID_ARG;
@@ -118,6 +123,8 @@ qd_status make_layout(const qd_config* c, qd_layout* L) {
   bytes[QD_BUF_BUCKET_ITEMS] = c->tess == QD_TESS_CVT ? (16 + 4) * C : 0;
   bytes[QD_BUF_CAND_COUNT] = 4 * (uint64_t)L->cand_buckets;
   bytes[QD_BUF_CAND_PTS] = 16 * (uint64_t)QD_CAND_SLOTS * (uint64_t)L->cand_buckets;
+  bytes[QD_BUF_LLOYD_ACC] =
+      c->tess == QD_TESS_CVT && c->cvt_samples > 0 && c->cvt_iters > 0 ? 8 * C * (D + 1) : 0;
   bytes[QD_BUF_ENV] = 4 * env;
   bytes[QD_BUF_OCC_LIST] = 4 * C;
   bytes[QD_BUF_COUNTERS] = 4 * 64;
@@ -311,6 +318,8 @@ qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
   p.cand_buckets = L->cand_buckets;
   p.cand_count = (int*)at(QD_BUF_CAND_COUNT);
   p.cand_pts = (float4*)at(QD_BUF_CAND_PTS);
+  p.cvt_samples = c->cvt_samples;
+  p.lloyd_acc = (unsigned long long*)at(QD_BUF_LLOYD_ACC);
   p.env = (float*)at(QD_BUF_ENV);
   p.occ_list = (int*)at(QD_BUF_OCC_LIST);
   p.counters = (int*)at(QD_BUF_COUNTERS);
@@ -358,6 +367,15 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
     go(qd::k_clear_archive, dim3(1024), dim3(256), p, 1);
     if (p.tess == qd::kTessCvt) {
       go(qd::k_centroids, dim3(blocks_for(p.C, 256)), dim3(256), p);
+      if (p.lloyd_acc) {
+        for (int it = 0; it < cfg->cvt_iters; ++it) {
+          const dim3 grid(blocks_for((uint64_t)p.cvt_samples, qd::kLloydBlock)), block(qd::kLloydBlock);
+          if (p.D == 2) go(qd::k_lloyd_assign<2>, grid, block, p);
+          else go(qd::k_lloyd_assign<4>, grid, block, p);
+          go(qd::k_lloyd_update, dim3(blocks_for(p.C, 256)), dim3(256), p);
+        }
+      }
+      go(qd::k_bucket_count, dim3(blocks_for(p.C, 256)), dim3(256), p);
       go(qd::k_bucket_scan, dim3(1), dim3(1024), p);
       go(qd::k_bucket_fill, dim3(blocks_for(p.C, 256)), dim3(256), p);
       if (p.cand_buckets > 0) go(qd::k_cand_build, dim3(blocks_for(p.cand_buckets, 256)), dim3(256), p);

@@ -15,15 +15,16 @@ from . import workloads as W
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqd.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 CAND_SLOTS = 16
 QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
     QD_ERR_UNSUPPORTED, QD_ERR_HIP = range(6)
 
 (BUF_ARCHIVE_KEY, BUF_ARCHIVE_FIT, BUF_ARCHIVE_DESC, BUF_ARCHIVE_SLOT, BUF_ARCHIVE_GENO,
- BUF_CENTROIDS, BUF_BUCKET_START, BUF_BUCKET_ITEMS, BUF_CAND_COUNT, BUF_CAND_PTS, BUF_ENV,
- BUF_OCC_LIST, BUF_COUNTERS, BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC, BUF_OFF_CELL,
- BUF_OFF_WON, BUF_OFF_KEY, BUF_OFF_BANK, BUF_OFF_GENO, BUF_STATS, NUM_BUFFERS) = range(23)
+ BUF_CENTROIDS, BUF_BUCKET_START, BUF_BUCKET_ITEMS, BUF_CAND_COUNT, BUF_CAND_PTS,
+ BUF_LLOYD_ACC, BUF_ENV, BUF_OCC_LIST, BUF_COUNTERS, BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC,
+ BUF_OFF_CELL, BUF_OFF_WON, BUF_OFF_KEY, BUF_OFF_BANK, BUF_OFF_GENO, BUF_STATS,
+ NUM_BUFFERS) = range(24)
 
 (K_VARY_EVAL, K_ROLLOUT, K_INSERT, K_REGEN, K_SETUP, NUM_KERNELS) = range(6)
 KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
@@ -43,7 +44,8 @@ class QdConfig(C.Structure):
         ("iso_sigma", C.c_float), ("line_sigma", C.c_float),
         ("init_lo", C.c_float), ("init_hi", C.c_float),
         ("mlp_obs", C.c_int32), ("mlp_hidden", C.c_int32), ("mlp_act", C.c_int32),
-        ("episode_len", C.c_int32), ("keep_offspring", C.c_int32), ("seed", C.c_uint64),
+        ("episode_len", C.c_int32), ("keep_offspring", C.c_int32),
+        ("cvt_samples", C.c_int32), ("cvt_iters", C.c_int32), ("seed", C.c_uint64),
     ]
 
 
@@ -122,6 +124,7 @@ def make_config(w: dict, keep_offspring: bool = False) -> QdConfig:
     c.init_lo, c.init_hi = w["init_lo"], w["init_hi"]
     c.mlp_obs, c.mlp_hidden, c.mlp_act, c.episode_len = w["obs"], w["hid"], w["act"], w["T"]
     c.keep_offspring = 1 if keep_offspring else 0
+    c.cvt_samples, c.cvt_iters = w.get("cvt_samples", 0), w.get("cvt_iters", 0)
     c.seed = w["seed"]
     return c
 

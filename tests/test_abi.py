@@ -89,9 +89,25 @@ def status_of(w, **cfg_over):
 @pytest.mark.parametrize("over", [
     dict(abi_version=99), dict(task=7), dict(tess=3), dict(batch_size=0), dict(num_cells=0),
     dict(genotype_dim=1), dict(desc_dim=3), dict(keep_offspring=2),
+    dict(cvt_samples=100, cvt_iters=1),          # Lloyd needs a CVT
 ])
 def test_invalid_configs(lib, over):
     assert status_of(W.workload("rastrigin_grid_b128"), **over) == Q.QD_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("over", [dict(cvt_samples=-1), dict(cvt_iters=-1),
+                                  dict(cvt_samples=(1 << 28) + 1), dict(cvt_iters=10001)])
+def test_invalid_lloyd(lib, over):
+    assert status_of(W.workload("rastrigin_proj_cvt_b65536"), **over) == Q.QD_ERR_INVALID_ARG
+
+
+def test_lloyd_accumulator_layout(lib):
+    w = W.workload("rastrigin_proj_cvt_b65536")
+    assert Q.layout_query(Q.make_config(w)).bytes[Q.BUF_LLOYD_ACC] == 0
+    lw = dict(w, cvt_samples=1000, cvt_iters=2)
+    assert Q.layout_query(Q.make_config(lw)).bytes[Q.BUF_LLOYD_ACC] == 8 * w["C"] * (w["D"] + 1)
+    nw = dict(w, cvt_samples=1000, cvt_iters=0)
+    assert Q.layout_query(Q.make_config(nw)).bytes[Q.BUF_LLOYD_ACC] == 0
 
 
 def test_invalid_grid_and_box(lib):

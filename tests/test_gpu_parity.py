@@ -60,13 +60,16 @@ SMALL = {
     # projection descriptors spread over the whole box: few genes drawn from the
     # full range, so the nearest-centroid search meets most fine buckets
     "proj_spread_cvt": dict(n=8, batch=3000, C=2000, init_lo=-5.12, init_hi=5.12, seed=3),
+    # the same on a Lloyd CVT (centroids moved by three Lloyd iterations)
+    "proj_spread_lloyd": dict(n=8, batch=2000, C=500, init_lo=-5.12, init_hi=5.12, seed=4,
+                              cvt_samples=20000, cvt_iters=3),
 }
 
 
 def small_workload(name):
     if name == "rastrigin_ragged":
         return W.workload("rastrigin_grid_b128", n=257, batch=77, seed=5)
-    if name == "proj_spread_cvt":
+    if name in ("proj_spread_cvt", "proj_spread_lloyd"):
         return W.workload("rastrigin_proj_cvt_b65536", **SMALL[name])
     return W.workload(name, **SMALL[name])
 
@@ -88,6 +91,25 @@ def test_first_batch_bit_exact(name):
     assert_archive_equal(a.snapshot(), o.archive(), o.n, "after the first batch")
     if w["tess"] == W.CVT:
         np.testing.assert_array_equal(a.views()["centroids"].cpu().numpy(), o.centroids())
+
+
+@pytest.mark.parametrize("C,D,S,L", [(64, 2, 3000, 5), (37, 4, 2000, 3), (1500, 2, 7777, 1),
+                                     (1000, 2, 20000, 2), (300, 4, 5000, 2)])
+def test_lloyd_centroids_bit_exact(C, D, S, L):
+    """Centroids after L Lloyd iterations over S points (several LDS tiles of
+    centroids, ragged point and tile counts) equal the oracle's."""
+    base = "rastrigin_proj_cvt_b65536" if D == 2 else "mlp64_cvt_b8192"
+    w = W.workload(base, C=C, batch=16, cvt_samples=S, cvt_iters=L, seed=2)
+    say(f"lloyd C={C} D={D} S={S} L={L}")
+    a = qd().Archive(w)
+    o = O.Oracle(w)
+    o.setup()
+    got = a.views()["centroids"].cpu().numpy()
+    np.testing.assert_array_equal(got, o.centroids())
+    plain = W.workload(base, C=C, batch=16, seed=2)
+    q = O.Oracle(plain)
+    q.setup()
+    assert np.any(got != q.centroids()), "Lloyd iterations moved no centroid"
 
 
 @pytest.mark.parametrize("C,seed", [(10000, 0), (2000, 3), (37, 1)])
