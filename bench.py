@@ -96,6 +96,9 @@ def main():
     ap.add_argument("--cvt-lloyd", type=int, nargs=2, metavar=("SAMPLES", "ITERS"),
                     help="build the CVT with Lloyd iterations over uniform points instead of "
                          "keeping the uniform centroids")
+    ap.add_argument("--death", nargs=2, metavar=("MODE", "BELOW"),
+                    help="policies: end episodes at failure (MODE 1 truncate, 2 discard) "
+                         "when new-state component 0 drops below BELOW")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run 3 plain device-to-device copies of MIB MiB (the reference "
                          "kernel for scaling HBM byte counters) and exit after them")
@@ -124,6 +127,8 @@ def main():
     w = W.workload(args.workload)
     if args.cvt_lloyd:
         w.update(cvt_samples=args.cvt_lloyd[0], cvt_iters=args.cvt_lloyd[1])
+    if args.death:
+        w.update(death_mode=int(args.death[0]), death_below=float(args.death[1]))
     n = W.genotype_len(w)
     nb = w["batch"]
     log(f"bench: workload {args.workload} N_B={nb} n={n} C={w['C']}; setting up")
@@ -199,7 +204,8 @@ def main():
                    "batch": nb, "genotype_dim": n, "cells": w["C"],
                    "tessellation": "grid" if w["tess"] == 0 else "cvt",
                    "episode_len": w["T"] if w["task"] == 3 else None, "seed": w["seed"],
-                   "cvt_lloyd": [w["cvt_samples"], w["cvt_iters"]] if w["cvt_iters"] else None},
+                   "cvt_lloyd": [w["cvt_samples"], w["cvt_iters"]] if w["cvt_iters"] else None,
+                   "death": [w["death_mode"], w["death_below"]] if w["death_mode"] else None},
         "setup_s": setup_s,                       # archive set-up and the first batch
         "paper_eval_per_s": paper_evals,          # second run, per-step events
         "median_step_ms": sorted(step_ms)[len(step_ms) // 2],

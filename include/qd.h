@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define QD_ABI_VERSION 3u
+#define QD_ABI_VERSION 4u
 
 /* Candidate slots per fine bucket of a two-dimensional CVT (see QD_BUF_CAND_*). */
 #define QD_CAND_SLOTS 16
@@ -76,6 +76,16 @@ typedef struct {
   int32_t cvt_iters;      /*   at set-up (0, 0: centroids stay uniform draws);    */
                           /*   0 <= cvt_samples <= 2^28, 0 <= cvt_iters <= 10^4,  */
                           /*   both 0 for the grid                                */
+  int32_t death_mode;     /* policies (Appendix A.3, A.4 i): 0 full episodes;    */
+                          /*   1 an episode ends at the first new state whose    */
+                          /*   component 0 is below death_below, that step and   */
+                          /*   the rest counting for nothing (return and         */
+                          /*   descriptor over the states before it); 2 as 1,    */
+                          /*   and every failed solution gets a NaN objective    */
+                          /*   (never inserted).  In 1 and 2 an episode with no  */
+                          /*   state before its failure gets a NaN objective and  */
+                          /*   descriptor 0.  Must be 0 for the test functions.  */
+  float death_below;      /*   the failure threshold (any non-NaN value)          */
   uint64_t seed;          /* key of every Philox4x32-10 stream                    */
 } qd_config;
 

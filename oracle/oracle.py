@@ -25,7 +25,8 @@ class OrConfig(C.Structure):
         ("iso_sigma", C.c_float), ("line_sigma", C.c_float),
         ("init_lo", C.c_float), ("init_hi", C.c_float),
         ("obs", C.c_int32), ("hid", C.c_int32), ("act", C.c_int32), ("T", C.c_int32),
-        ("cvt_samples", C.c_int32), ("cvt_iters", C.c_int32), ("seed", C.c_uint64),
+        ("cvt_samples", C.c_int32), ("cvt_iters", C.c_int32),
+        ("death_mode", C.c_int32), ("death_below", C.c_float), ("seed", C.c_uint64),
     ]
 
 
@@ -59,7 +60,7 @@ def lib():
             "or_grid_cell": (C.c_int32, [f32p, C.c_int32, i32p, f32p, f32p]),
             "or_cvt_cell": (C.c_int32, [f32p, C.c_int32, f32p, f32p, f32p, C.c_int32]),
             "or_mlp_rollout": (None, [f32p, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                      f32p, f32p, f32p, f32p, f32p]),
+                                      f32p, f32p, f32p, C.c_int32, C.c_float, f32p, f32p]),
             "or_key": (C.c_uint64, [C.c_float, C.c_int32, C.c_int32]),
             "or_map_f32": (None, [C.c_int32, f32p, f32p, C.c_int64]),
             "or_philox_many": (None, [u32p, u32p, u32p, C.c_int64]),
@@ -108,6 +109,7 @@ def make_config(w: dict) -> OrConfig:
     c.init_lo, c.init_hi = w["init_lo"], w["init_hi"]
     c.obs, c.hid, c.act, c.T = w["obs"], w["hid"], w["act"], w["T"]
     c.cvt_samples, c.cvt_iters = w.get("cvt_samples", 0), w.get("cvt_iters", 0)
+    c.death_mode, c.death_below = w.get("death_mode", 0), w.get("death_below", 0.0)
     c.seed = w["seed"]
     return c
 
@@ -209,7 +211,7 @@ def cvt_cell(d, lo, hi, cent) -> int:
                              _ptr(hi_a, C.c_float), _ptr(cent, C.c_float), cent.shape[0])
 
 
-def mlp_rollout(w, obs, hid, act, T, A, B, s0):
+def mlp_rollout(w, obs, hid, act, T, A, B, s0, death_mode=0, death_below=0.0):
     w = np.ascontiguousarray(np.asarray(w, dtype=np.float32))
     A = np.ascontiguousarray(np.asarray(A, dtype=np.float32))
     B = np.ascontiguousarray(np.asarray(B, dtype=np.float32))
@@ -217,8 +219,8 @@ def mlp_rollout(w, obs, hid, act, T, A, B, s0):
     fit = np.zeros(1, np.float32)
     desc = np.zeros(4, np.float32)
     lib().or_mlp_rollout(_ptr(w, C.c_float), obs, hid, act, T, _ptr(A, C.c_float),
-                         _ptr(B, C.c_float), _ptr(s0, C.c_float), _ptr(fit, C.c_float),
-                         _ptr(desc, C.c_float))
+                         _ptr(B, C.c_float), _ptr(s0, C.c_float), death_mode, death_below,
+                         _ptr(fit, C.c_float), _ptr(desc, C.c_float))
     return fit[0], desc
 
 

@@ -441,9 +441,17 @@ static void dense_tanh_sliced8(const float* W, const float* bias, const float* i
   }
 }
 
+/* Failure (Appendix A.3, A.4 i): with death_mode != 0 the episode stops at
+ * the first step whose new state has component 0 below death_below; that step
+ * and the rest count for nothing, so the return and the descriptor cover only
+ * the states before the failure (a variable-length episode; the descriptor
+ * is the mean over those states).  death_mode 2 also discards every failed
+ * solution, and an episode with no state before its failure is discarded in
+ * both modes: a discarded solution gets a NaN objective, which insertion
+ * never accepts (the death flag). */
 void or_mlp_rollout(const float* w, int32_t obs, int32_t hid, int32_t act, int32_t T,
-                    const float* A, const float* B, const float* s0, float* fit,
-                    float* desc) {
+                    const float* A, const float* B, const float* s0, int32_t death_mode,
+                    float death_below, float* fit, float* desc) {
   const float* W1 = w;
   const float* b1 = W1 + (size_t)hid * obs;
   const float* W2 = b1 + hid;
@@ -458,6 +466,7 @@ void or_mlp_rollout(const float* w, int32_t obs, int32_t hid, int32_t act, int32
   for (int32_t i = 0; i < obs; ++i) s[i] = s0[i];
   float ret = 0.0f;
   float dsum[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  int32_t valid = 0, failed = 0;
   for (int32_t t = 0; t < T; ++t) {
     dense_tanh(W1, b1, s, obs, hid, h1);
     dense_tanh(W2, b2, h1, hid, hid, h2);
@@ -468,14 +477,19 @@ void or_mlp_rollout(const float* w, int32_t obs, int32_t hid, int32_t act, int32
       for (int32_t k = 0; k < act; ++k) ba = fmaf(B[(size_t)i * act + k], a[k], ba);
       sn[i] = or_tanhf(as + ba);
     }
+    if (death_mode != 0 && sn[0] < death_below) {
+      failed = 1;
+      break;
+    }
     float q = 0.0f;
     for (int32_t o = 0; o < act; ++o) q = fmaf(a[o], a[o], q);
     ret = ret + fmaf(-0.5f, q, sn[0]);
     for (int32_t k = 0; k < 4; ++k) dsum[k] = dsum[k] + or_sigmoidf(sn[1 + k]);
     for (int32_t i = 0; i < obs; ++i) s[i] = sn[i];
+    valid += 1;
   }
-  *fit = ret;
-  for (int32_t k = 0; k < 4; ++k) desc[k] = dsum[k] / (float)T;
+  *fit = ((death_mode == 2 && failed) || valid == 0) ? NAN : ret;
+  for (int32_t k = 0; k < 4; ++k) desc[k] = valid > 0 ? dsum[k] / (float)valid : 0.0f;
   free(s);
 }
 
@@ -659,7 +673,8 @@ static void evaluate(const or_state* s, const float* x, float* fit, float* desc)
     const float* A = s->env;
     const float* B = A + (size_t)c->obs * c->obs;
     const float* s0 = B + (size_t)c->obs * c->act;
-    or_mlp_rollout(x, c->obs, c->hid, c->act, c->T, A, B, s0, fit, desc);
+    or_mlp_rollout(x, c->obs, c->hid, c->act, c->T, A, B, s0, c->death_mode, c->death_below,
+                   fit, desc);
   } else {
     or_eval_testfn(c->task, x, s->n, c->lo, c->hi, fit, desc);
   }

@@ -33,6 +33,8 @@ typedef struct {
   int32_t obs, hid, act, T;   /* MLP policy and rollout                         */
   int32_t cvt_samples;  /* CVT: Lloyd iterations over this many uniform points  */
   int32_t cvt_iters;    /*      (0 = centroids stay the uniform draws)          */
+  int32_t death_mode;   /* policies: 0 none, 1 truncate at failure, 2 discard   */
+  float death_below;    /*   failure: new state component 0 below this          */
   uint64_t seed;
 } or_config;
 
@@ -58,8 +60,8 @@ int32_t  or_grid_cell(const float* d, int32_t D, const int32_t* grid, const floa
 int32_t  or_cvt_cell(const float* d, int32_t D, const float* lo, const float* hi,
                      const float* cent, int32_t C);
 void     or_mlp_rollout(const float* w, int32_t obs, int32_t hid, int32_t act, int32_t T,
-                        const float* A, const float* B, const float* s0, float* fit,
-                        float* desc);
+                        const float* A, const float* B, const float* s0, int32_t death_mode,
+                        float death_below, float* fit, float* desc);
 uint64_t or_key(float f, int32_t j, int32_t batch);
 void     or_map_f32(int32_t fn, const float* in, float* out, int64_t count);
 void     or_philox_many(const uint32_t* ctr, const uint32_t key[2], uint32_t* out,

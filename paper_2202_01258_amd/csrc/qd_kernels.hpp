@@ -49,6 +49,8 @@ struct Params {
   int* bucket_start;              // [num_buckets + 1], then [num_buckets] cursors
   float4* bucket_pts;             // [C]
   int* bucket_idx;                // [C]
+  int death_mode;                 // policies: 0 none, 1 truncate, 2 discard failed
+  float death_below;              // failure: new state component 0 below this
   int cvt_samples;                // Lloyd points (set-up only)
   unsigned long long* lloyd_acc;  // [C][D + 1]: coordinate numerator sums, count
   int cand_res, cand_buckets;     // D = 2 CVT fine buckets (0: none)

@@ -60,6 +60,9 @@ qd_status validate(const qd_config* c) {
     return QD_ERR_INVALID_ARG;
   if (c->tess == QD_TESS_GRID && (c->cvt_samples != 0 || c->cvt_iters != 0))
     return QD_ERR_INVALID_ARG;
+  if (c->death_mode < 0 || c->death_mode > 2 || (c->death_mode != 0 && !is_mlp(c)) ||
+      c->death_below != c->death_below)
+    return QD_ERR_INVALID_ARG;
   const int D = c->desc_dim;
   if (is_mlp(c)) {
     if (c->genotype_dim != 0 || D != 4) return QD_ERR_INVALID_ARG;
@@ -318,6 +321,8 @@ qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
   p.cand_buckets = L->cand_buckets;
   p.cand_count = (int*)at(QD_BUF_CAND_COUNT);
   p.cand_pts = (float4*)at(QD_BUF_CAND_PTS);
+  p.death_mode = c->death_mode;
+  p.death_below = c->death_below;
   p.cvt_samples = c->cvt_samples;
   p.lloyd_acc = (unsigned long long*)at(QD_BUF_LLOYD_ACC);
   p.env = (float*)at(QD_BUF_ENV);

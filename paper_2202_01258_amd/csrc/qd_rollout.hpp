@@ -132,6 +132,7 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   __shared__ float s_h1[H];
   __shared__ float s_h2[H];
   __shared__ float s_a[A];
+  __shared__ int s_fail;
 
   __shared__ float2 s_turn[256], s_logt[128];
 
@@ -190,11 +191,13 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     for (int k = 0; k < A; ++k) brow[k] = envB[o * A + k];
     s_state[0][o] = envS[o];
   }
+  if (o == 0) s_fail = 0;
   __syncthreads();
 
-  // ---- episode
+  // ---- episode; with death_mode != 0 it ends at the first new state whose
+  // component 0 is below death_below, and that step counts for nothing
   float ret = 0.0f, dsum = 0.0f;
-  int cur = 0;
+  int cur = 0, valid = 0;
   for (int step = 0; step < p.T; ++step) {
     const float* s = s_state[cur];
     const float z1 = dot4<O>(w1, s) + b1v;
@@ -221,7 +224,13 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
       for (int k = 0; k < A; ++k) ba = fma32(brow[k], s_a[k], ba);
       const float sn = tanh32(as + ba);
       s_state[cur ^ 1][o] = sn;
-      if (o == 0) {
+      // lane 0 holds component 0 of the new state (lanes 0..26 share wave 0)
+      const bool fail = p.death_mode != 0 &&
+                        __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(sn), 0)) <
+                            p.death_below;
+      if (fail) {
+        if (o == 0) s_fail = 1;
+      } else if (o == 0) {
         float qa = 0.0f;
 #pragma unroll
         for (int k = 0; k < A; ++k) qa = fma32(s_a[k], s_a[k], qa);
@@ -232,15 +241,19 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
     }
     cur ^= 1;
     __syncthreads();
+    if (s_fail) break;   // the same value in every thread after the barrier
+    ++valid;
   }
+  // death flag (Appendix A.4 i): a NaN objective is never inserted
+  const bool dead = (p.death_mode == 2 && s_fail) || valid == 0;
   if (o == 0) {
-    p.off_fit[j] = ret;
+    p.off_fit[j] = dead ? __builtin_nanf("") : ret;
     p.off_par[2 * j] = q.c1;
     p.off_par[2 * j + 1] = q.c2;
     p.off_bank[j] = (uint8_t)q.banks;
     p.off_won[j] = 0;
   } else if (o <= 4) {
-    p.off_desc[(size_t)j * 4 + (o - 1)] = dsum / (float)p.T;
+    p.off_desc[(size_t)j * 4 + (o - 1)] = valid > 0 ? dsum / (float)valid : 0.0f;
   }
 }
 

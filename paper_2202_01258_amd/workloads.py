@@ -23,7 +23,7 @@ _BASE = dict(
     task=RASTRIGIN, tess=GRID, n=100, batch=128, D=2, grid=(100, 100), C=10000,
     lo=(-5.12, -5.12), hi=(5.12, 5.12), iso_sigma=0.005, line_sigma=0.05,
     init_lo=-0.1, init_hi=0.1, obs=27, hid=64, act=8, T=250, seed=0, generations=100,
-    cvt_samples=0, cvt_iters=0,
+    cvt_samples=0, cvt_iters=0, death_mode=0, death_below=0.0,
 )
 
 WORKLOADS = {

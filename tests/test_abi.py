@@ -90,6 +90,7 @@ def status_of(w, **cfg_over):
     dict(abi_version=99), dict(task=7), dict(tess=3), dict(batch_size=0), dict(num_cells=0),
     dict(genotype_dim=1), dict(desc_dim=3), dict(keep_offspring=2),
     dict(cvt_samples=100, cvt_iters=1),          # Lloyd needs a CVT
+    dict(death_mode=1),                          # death flags are for policies
 ])
 def test_invalid_configs(lib, over):
     assert status_of(W.workload("rastrigin_grid_b128"), **over) == Q.QD_ERR_INVALID_ARG
@@ -99,6 +100,17 @@ def test_invalid_configs(lib, over):
                                   dict(cvt_samples=(1 << 28) + 1), dict(cvt_iters=10001)])
 def test_invalid_lloyd(lib, over):
     assert status_of(W.workload("rastrigin_proj_cvt_b65536"), **over) == Q.QD_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("over", [dict(death_mode=3), dict(death_mode=-1),
+                                  dict(death_mode=1, death_below=float("nan"))])
+def test_invalid_death(lib, over):
+    assert status_of(W.workload("mlp64_cvt_b8192"), **over) == Q.QD_ERR_INVALID_ARG
+
+
+def test_death_modes_accepted(lib):
+    for mode in (0, 1, 2):
+        assert status_of(W.workload("mlp64_cvt_b8192"), death_mode=mode, death_below=-0.5) == Q.QD_OK
 
 
 def test_lloyd_accumulator_layout(lib):

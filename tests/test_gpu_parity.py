@@ -269,15 +269,24 @@ def test_full_size_rastrigin_projection_sampled(batch):
 
 
 MLP_SMALL = {
-    "mlp64_cvt_b8192": dict(batch=48, T=250),
-    "mlp128_cvt_b65536": dict(batch=16, T=40, C=500),
+    "mlp64_cvt_b8192": ("mlp64_cvt_b8192", dict(batch=48, T=250)),
+    "mlp128_cvt_b65536": ("mlp128_cvt_b65536", dict(batch=16, T=40, C=500)),
+    # failure at new-state component 0 < -0.07: about a third of the first
+    # batch fails, most at the first step, some within the episode
+    "mlp64_death_truncate": ("mlp64_cvt_b8192",
+                             dict(batch=64, T=60, death_mode=1, death_below=-0.07)),
+    "mlp64_death_discard": ("mlp64_cvt_b8192",
+                            dict(batch=64, T=60, death_mode=2, death_below=-0.07)),
+    "mlp128_death_truncate": ("mlp128_cvt_b65536",
+                              dict(batch=24, T=40, C=500, death_mode=1, death_below=-0.07)),
 }
 
 
 @pytest.mark.parametrize("name", list(MLP_SMALL))
 def test_mlp_bit_exact(name):
-    w = W.workload(name, **MLP_SMALL[name])
-    say(f"mlp {name} {MLP_SMALL[name]}: first batch")
+    base, kw = MLP_SMALL[name]
+    w = W.workload(base, **kw)
+    say(f"mlp {name} {kw}: first batch")
     a = qd().Archive(w, keep_offspring=True)
     o = O.Oracle(w)
     o.init()
@@ -288,6 +297,7 @@ def test_mlp_bit_exact(name):
     np.testing.assert_array_equal(gb["desc"], ob["desc"])
     np.testing.assert_array_equal(gb["cell"], ob["cell"])
     assert_archive_equal(a.snapshot(), o.archive(), o.n, "first batch")
+    deaths = int(np.isnan(gb["fit"]).sum())
     for g in (1, 2, 3):
         say(f"mlp {name}: generation {g}")
         a.generation(g)
@@ -299,6 +309,9 @@ def test_mlp_bit_exact(name):
         np.testing.assert_array_equal(gb["won"], ob["won"])
         assert_archive_equal(a.snapshot(), o.archive(), o.n, f"generation {g}")
     assert a.stats()["qd_score"] == pytest.approx(o.stats()["qd_score"], rel=1e-12)
+    if w.get("death_mode", 0):
+        # the failure rule was exercised: the first batch holds death flags
+        assert deaths > 0
 
 
 @pytest.mark.parametrize("name,batch,samples", [("mlp64_cvt_b8192", 8192, 6),
