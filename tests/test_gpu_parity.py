@@ -349,7 +349,8 @@ def test_mlp_full_size_sampled(name, batch, samples):
 
 
 @pytest.mark.parametrize("kw", [dict(batch=1), dict(n=2, batch=5), dict(n=101, batch=9),
-                                dict(C=1, grid=(1, 1), batch=33)])
+                                dict(C=1, grid=(1, 1), batch=33),
+                                dict(n=65537, batch=6)])     # long rows with a ragged tail
 def test_edge_shapes(kw):
     w = W.workload("rastrigin_grid_b128", **kw)
     say(f"edge shape {kw}")
@@ -361,6 +362,30 @@ def test_edge_shapes(kw):
         o.generation(g)
         np.testing.assert_array_equal(a.last_batch()["geno"], o.last_offspring())
     assert_archive_equal(a.snapshot(), o.archive(), o.n, f"{kw}")
+
+
+def test_empty_archive_sets_the_flag_and_inserts_nothing():
+    """Every first-batch policy fails at once (death flags): the archive stays
+    empty, and the next generation reports the empty archive (flag bit 0)
+    instead of selecting parents, with every offspring marked not inserted."""
+    w = W.workload("mlp64_cvt_b8192", batch=16, T=5, C=64, death_mode=2,
+                   death_below=float("inf"))
+    say("empty archive")
+    a = qd().Archive(w)
+    st = a.stats()
+    assert st["num_occupied"] == 0 and st["flags"] == 0 and np.isnan(st["best"])
+    assert np.isnan(a.last_batch()["fit"]).all()
+    o = O.Oracle(w)
+    o.init()
+    assert o.stats()["coverage"] == 0
+    a.generation(1)
+    gb = a.last_batch()
+    assert np.isnan(gb["fit"]).all()
+    assert (gb["parents"] == -1).all() and (gb["cell"] == -1).all() and not gb["won"].any()
+    st = a.stats()
+    assert st["num_occupied"] == 0 and st["flags"] & 1
+    with pytest.raises(RuntimeError, match="empty archive"):
+        o.generation(1)                   # the oracle finds no parent either
 
 
 def test_fast_division_and_sqrt_equal_ieee_on_all_inputs():
