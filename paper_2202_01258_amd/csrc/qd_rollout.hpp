@@ -77,6 +77,86 @@ __device__ __forceinline__ float dot4(const float* w, const float* x) {
   return (p0 + p2) + (p1 + p3);
 }
 
+// The same sums with the inputs broadcast from registers instead of LDS.
+// With the DPP control row_newbcast:m, the first source of v_fmac_f32 is
+// read from lane m of the executing lane's row of 16.  Component t of `v`
+// holds, in lane 16 r + m, input 4 m + t of a run of 64 inputs (the same in
+// every row r), so broadcast m of component t is input 4 m + t in every lane,
+// and each partial sum below still takes its inputs in ascending order.  One
+// float4 per lane per run replaces sixteen wave-wide LDS broadcasts.
+// The compiler does not fold a DPP move into v_fmac, hence the asm.  No VGPR
+// operand of a DPP instruction may be written by either of the two
+// instructions before it: every block opens with s_nop 1, and inside a block
+// each accumulator is written four instructions before it is read again.  The
+// blocks must run with every lane of the wave active.
+#define QD_BROW(B, W0, W1, W2, W3)                                                     \
+  "v_fmac_f32_dpp %0, %4, %" #W0 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t" \
+  "v_fmac_f32_dpp %1, %5, %" #W1 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t" \
+  "v_fmac_f32_dpp %2, %6, %" #W2 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t" \
+  "v_fmac_f32_dpp %3, %7, %" #W3 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t"
+#define QD_BROW3(B, W0, W1, W2)                                                        \
+  "v_fmac_f32_dpp %0, %4, %" #W0 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t" \
+  "v_fmac_f32_dpp %1, %5, %" #W1 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t" \
+  "v_fmac_f32_dpp %2, %6, %" #W2 " row_newbcast:" #B " row_mask:0xf bank_mask:0xf\n\t"
+#define QD_BFMA_IO(w)                                                                   \
+  : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3])                             \
+  : "v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w), "v"(w[0]), "v"(w[1]), "v"(w[2]), "v"(w[3]), \
+    "v"(w[4]), "v"(w[5]), "v"(w[6]), "v"(w[7]), "v"(w[8]), "v"(w[9]), "v"(w[10])
+#define QD_BFMA_IO16(w)                                                                 \
+  QD_BFMA_IO(w), "v"(w[11]), "v"(w[12]), "v"(w[13]), "v"(w[14]), "v"(w[15])
+
+// Inputs 16 B .. 16 B + 15 of a run (broadcasts 4 B .. 4 B + 3), weights w[0 .. 16).
+template <int B>
+__device__ __forceinline__ void bfma16(float (&acc)[4], const float4& v, const float* w) {
+  if constexpr (B == 0) {
+    __asm__("s_nop 1\n\t" QD_BROW(0, 8, 9, 10, 11) QD_BROW(1, 12, 13, 14, 15)
+                QD_BROW(2, 16, 17, 18, 19) QD_BROW(3, 20, 21, 22, 23) QD_BFMA_IO16(w));
+  } else if constexpr (B == 1) {
+    __asm__("s_nop 1\n\t" QD_BROW(4, 8, 9, 10, 11) QD_BROW(5, 12, 13, 14, 15)
+                QD_BROW(6, 16, 17, 18, 19) QD_BROW(7, 20, 21, 22, 23) QD_BFMA_IO16(w));
+  } else if constexpr (B == 2) {
+    __asm__("s_nop 1\n\t" QD_BROW(8, 8, 9, 10, 11) QD_BROW(9, 12, 13, 14, 15)
+                QD_BROW(10, 16, 17, 18, 19) QD_BROW(11, 20, 21, 22, 23) QD_BFMA_IO16(w));
+  } else {
+    static_assert(B == 3, "four blocks per run");
+    __asm__("s_nop 1\n\t" QD_BROW(12, 8, 9, 10, 11) QD_BROW(13, 12, 13, 14, 15)
+                QD_BROW(14, 16, 17, 18, 19) QD_BROW(15, 20, 21, 22, 23) QD_BFMA_IO16(w));
+  }
+}
+
+// Inputs 16 .. 26 of a run (broadcasts 4, 5 and 6 without input 27), weights w[0 .. 11).
+__device__ __forceinline__ void bfma11(float (&acc)[4], const float4& v, const float* w) {
+  __asm__("s_nop 1\n\t" QD_BROW(4, 8, 9, 10, 11) QD_BROW(5, 12, 13, 14, 15)
+              QD_BROW3(6, 16, 17, 18) QD_BFMA_IO(w));
+}
+
+// dot4<N> for N a multiple of 64; run r of x is read as one float4 per lane
+// from x + 64 r + 4 (lane mod 16), 16-byte aligned.
+template <int N>
+__device__ __forceinline__ float dot4_bcast(const float* w, const float* x) {
+  static_assert(N % 64 == 0, "whole runs of 64 inputs");
+  const int m = (int)(threadIdx.x & 15);
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int r = 0; r < N / 64; ++r) {
+    const float4 v = *reinterpret_cast<const float4*>(x + 64 * r + 4 * m);
+    bfma16<0>(acc, v, w + 64 * r);
+    bfma16<1>(acc, v, w + 64 * r + 16);
+    bfma16<2>(acc, v, w + 64 * r + 32);
+    bfma16<3>(acc, v, w + 64 * r + 48);
+  }
+  return (acc[0] + acc[2]) + (acc[1] + acc[3]);
+}
+
+// dot4<27> on `v`, the float4 a lane reads from x + 4 (lane mod 8) of a
+// 32-float, 16-byte aligned x (its input 27 and broadcast 7 are never used).
+__device__ __forceinline__ float dot4_bcast27(const float* w, const float4& v) {
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  bfma16<0>(acc, v, w);
+  bfma11(acc, v, w + 16);
+  return (acc[0] + acc[2]) + (acc[1] + acc[3]);
+}
+
 __device__ __forceinline__ float pick4(const float4& v, int k) {
   return k == 0 ? v.x : (k == 1 ? v.y : (k == 2 ? v.z : v.w));
 }
@@ -128,8 +208,8 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   constexpr int O = kObs, A = kAct, SL = H / 8;
   constexpr int E1 = H * O, E2 = E1 + H, E3 = E2 + H * H, E4 = E3 + H;   // W3 at E4, b3 after
   constexpr int OUT_WAVE_FIRST = H - 64;                                  // first lane of it
-  __shared__ float s_state[2][32];
-  __shared__ float s_h1[H];
+  __shared__ __attribute__((aligned(16))) float s_state[2][32];
+  __shared__ __attribute__((aligned(16))) float s_h1[H];
   __shared__ float s_h2[H];
   __shared__ float s_a[A];
   __shared__ int s_fail;
@@ -184,6 +264,8 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   const float* envA = p.env;
   const float* envB = p.env + O * O;
   const float* envS = p.env + O * O + O * A;
+#pragma unroll
+  for (int k = 0; k < O; ++k) arow[k] = 0.0f;
   if (o < O) {
 #pragma unroll
     for (int k = 0; k < O; ++k) arow[k] = envA[o * O + k];
@@ -199,13 +281,14 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   float ret = 0.0f, dsum = 0.0f;
   int cur = 0, valid = 0;
   for (int step = 0; step < p.T; ++step) {
-    const float* s = s_state[cur];
-    const float z1 = dot4<O>(w1, s) + b1v;
+    static_assert(O == 27, "the state is read as broadcasts 0 .. 6 of one float4");
+    const float4 sv = *reinterpret_cast<const float4*>(&s_state[cur][4 * (o & 7)]);
+    const float z1 = dot4_bcast27(w1, sv) + b1v;
     float as = 0.0f;
-    if (o < O) as = dot4<O>(arow, s);
+    if (o < 64) as = dot4_bcast27(arow, sv);   // all of wave 0 (lanes 0 .. O-1 use it)
     s_h1[o] = tanh32(z1);
     __syncthreads();
-    const float z2 = dot4<H>(w2, s_h1) + b2v;
+    const float z2 = dot4_bcast<H>(w2, s_h1) + b2v;
     s_h2[o] = tanh32(z2);
     __syncthreads();
     if (out_lane) {
