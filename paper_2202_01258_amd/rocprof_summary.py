@@ -8,12 +8,11 @@
           <copy_fetch.db> <copy_write.db> <fetch.db> <write.db> --copy-mib M
       HBM bytes per launch of KERNEL: FETCH_SIZE and WRITE_SIZE (KiB per
       dispatch) each scaled by bytes moved / counter value of a plain copy of
-      M MiB, with a digest of the kernel sources the counters belong to
+      M MiB, with a digest of the sources that kernel is built from
 """
 from __future__ import annotations
 
 import argparse
-import glob
 import hashlib
 import os
 import sqlite3
@@ -21,15 +20,26 @@ import sqlite3
 TRAFFIC_TAG = "traffic_bytes_per_launch"
 
 
-def sources_digest() -> str:
-    """sha256 over the HIP sources and the public header, in name order."""
+# Sources a kernel's code depends on: every kernel is built from the device
+# helpers, the kernel header, the launch code and the build flags; the policy
+# kernels also from the rollout header.
+_COMMON = ["csrc/qd_device.hpp", "csrc/qd_kernels.hpp", "csrc/qd_lib.hip", "build.py",
+           "../include/qd.h"]
+_POLICY = ["csrc/qd_rollout.hpp"]
+
+
+def sources_digest(kernel: str) -> str:
+    """sha256 over the sources `kernel` (a demangled name) is built from, in
+    name order; counters taken on other sources do not describe it."""
     root = os.path.dirname(os.path.abspath(__file__))
-    files = sorted(glob.glob(os.path.join(root, "csrc", "*")))
-    files.append(os.path.join(os.path.dirname(root), "include", "qd.h"))
+    names = list(_COMMON)
+    if kernel.startswith(("k_rollout", "k_regen_mlp")):
+        names += _POLICY
     h = hashlib.sha256()
-    for f in files:
-        h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
+    for rel in sorted(names):
+        path = os.path.normpath(os.path.join(root, rel))
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
@@ -39,7 +49,7 @@ def recorded_traffic(summary_path: str, kernel: str) -> float | None:
     when the file is absent or was taken on other kernel sources."""
     if not os.path.exists(summary_path):
         return None
-    want = sources_digest()
+    want = sources_digest(kernel)
     with open(summary_path) as fh:
         for line in fh:
             parts = line.split(maxsplit=3)
@@ -98,7 +108,7 @@ def traffic(kernel: str, copy_fetch: str, copy_write: str, fetch: str, write: st
         f"WRITE_SIZE {cw:.1f} KiB -> scale {w_scale:.4f}",
         f"{kernel}: FETCH_SIZE {kf:.2f} KiB/dispatch ({nf} dispatches) -> {rd:.0f} B read; "
         f"WRITE_SIZE {kw:.2f} KiB/dispatch ({nw} dispatches) -> {wr:.0f} B written",
-        f"{TRAFFIC_TAG} {rd + wr:.0f} {sources_digest()} {kernel}",
+        f"{TRAFFIC_TAG} {rd + wr:.0f} {sources_digest(kernel)} {kernel}",
     ])
 
 

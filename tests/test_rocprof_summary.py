@@ -1,0 +1,36 @@
+"""Host logic of the profile summaries: the recorded HBM traffic is used only
+while the sources its kernel is built from are unchanged."""
+import os
+
+from paper_2202_01258_amd import rocprof_summary as R
+
+VARY = "k_vary_eval<2, false, false>"
+ROLL = "k_rollout<64, false, false>"
+
+
+def test_digest_covers_the_rollout_header_only_for_policy_kernels():
+    assert R.sources_digest(VARY) == R.sources_digest("k_insert<1, 2>")
+    assert R.sources_digest(VARY) != R.sources_digest(ROLL)
+    assert R.sources_digest(ROLL) == R.sources_digest("k_regen_mlp<false>")
+
+
+def test_recorded_traffic_matches_kernel_and_digest(tmp_path):
+    f = tmp_path / "t.txt"
+    f.write_text("header line\n"
+                 f"{R.TRAFFIC_TAG} 1234 {R.sources_digest(VARY)} {VARY}\n"
+                 f"{R.TRAFFIC_TAG} 99 {'0' * 64} {ROLL}\n")
+    assert R.recorded_traffic(str(f), VARY) == 1234.0
+    assert R.recorded_traffic(str(f), ROLL) is None          # other sources
+    assert R.recorded_traffic(str(f), "k_other") is None     # not recorded
+    assert R.recorded_traffic(str(tmp_path / "absent.txt"), VARY) is None
+
+
+def test_committed_summaries_name_their_kernel():
+    root = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "profiles")
+    for name in os.listdir(root):
+        if not name.endswith("_hbm_traffic.txt"):
+            continue
+        with open(os.path.join(root, name)) as fh:
+            tagged = [ln.split(maxsplit=3) for ln in fh if ln.startswith(R.TRAFFIC_TAG)]
+        assert len(tagged) == 1, name
+        assert name.startswith(tagged[0][3].split("<")[0].strip()), name
