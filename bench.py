@@ -91,7 +91,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="rastrigin_proj_cvt_b65536")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-generations", type=int, default=2)
+    ap.add_argument("--cpu-generations", type=int, default=4)
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--cvt-lloyd", type=int, nargs=2, metavar=("SAMPLES", "ITERS"),
                     help="build the CVT with Lloyd iterations over uniform points instead of "
