@@ -193,6 +193,50 @@ __device__ __forceinline__ void mlp_genes_run(const Params& p, const Pair& q, ui
   }
 }
 
+// Steps a rollout records for its reward and descriptor sums (see k_rollout).
+constexpr int kRing = 64;
+
+// Orders the LDS accesses of one wave's lanes around this point.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// Folds the first m ring slots into the running sums; called by all 64
+// lanes of wave 0.  Lane i < m turns slot i into its step's reward
+// s'_0 - 0.5 |a|^2 (|a|^2 as an fma chain over the actions in order) and the
+// sigmoids of s'_1 .. s'_4; then lane 0 adds the m rewards and lanes 1 .. 4
+// their m sigmoids to `acc`, in slot (= step) order -- the same operations in
+// the same order as adding each step's terms as the step ends.
+template <int A>
+__device__ __forceinline__ void flush_ring(float (*ra)[A], float (*rs)[kRing + 1], int m, int o,
+                                           float& acc) {
+  wave_sync();
+  if (o < m) {
+    float qa = 0.0f;
+#pragma unroll
+    for (int k = 0; k < A; ++k) qa = fma32(ra[o][k], ra[o][k], qa);
+    rs[0][o] = fma32(-0.5f, qa, rs[0][o]);
+#pragma unroll 1
+    for (int c = 1; c <= 4; ++c) rs[c][o] = sigmoid32(rs[c][o]);
+  }
+  wave_sync();
+  if (o <= 4) {
+    const float* row = rs[o];
+    int i = 0;
+    for (; i + 8 <= m; i += 8) {   // eight loads in flight, then eight adds
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = row[i + t];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc = acc + v[t];
+    }
+    for (; i < m; ++i) acc = acc + row[i];
+  }
+  wave_sync();
+}
+
 // One individual per workgroup of H threads (H / 64 waves):
 //   thread o      row o of W1 and W2, b1[o], b2[o] in VGPRs; hidden neuron o
 //   thread i < 27 row i of A and B (shared environment) in VGPRs; state i
@@ -203,15 +247,22 @@ __device__ __forceinline__ void mlp_genes_run(const Params& p, const Pair& q, ui
 //                 waves.
 // Per step: layer 1 and the A s product, layer 2, output layer, B a product
 // and the new state; activations pass through LDS with one barrier per stage.
+// The reward and the descriptor's sigmoids, which only lanes 0 .. 4 need,
+// are not evaluated in the step: the step's actions and new-state components
+// 0 .. 4 go to a ring in LDS, folded in every kRing steps by all of wave 0.
 template <int H, bool GEN0, bool KEEP>
-__global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
+__global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, uint32_t g) {
   constexpr int O = kObs, A = kAct, SL = H / 8;
   constexpr int E1 = H * O, E2 = E1 + H, E3 = E2 + H * H, E4 = E3 + H;   // W3 at E4, b3 after
   constexpr int OUT_WAVE_FIRST = H - 64;                                  // first lane of it
   __shared__ __attribute__((aligned(16))) float s_state[2][32];
   __shared__ __attribute__((aligned(16))) float s_h1[H];
   __shared__ float s_h2[H];
-  __shared__ float s_a[A];
+  // Ring of the last kRing valid steps: their actions, and their new states'
+  // components 0 .. 4 (later the step's reward and four sigmoids).  Rows are
+  // padded so that lanes 0 .. 4 reading one column hit different banks.
+  __shared__ __attribute__((aligned(16))) float s_ra[kRing][A];
+  __shared__ float s_rs[5][kRing + 1];
   __shared__ int s_fail;
 
   __shared__ float2 s_turn[256], s_logt[128];
@@ -277,10 +328,14 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
   __syncthreads();
 
   // ---- episode; with death_mode != 0 it ends at the first new state whose
-  // component 0 is below death_below, and that step counts for nothing
-  float ret = 0.0f, dsum = 0.0f;
+  // component 0 is below death_below, and that step counts for nothing.
+  // Lane 0 sums the rewards, lanes 1 .. 4 the sigmoids of state components
+  // 1 .. 4, each in step order; both are worked out from the ring, kRing
+  // steps at a time (flush_ring), not inside the step.
+  float acc = 0.0f;
   int cur = 0, valid = 0;
   for (int step = 0; step < p.T; ++step) {
+    const int slot = valid & (kRing - 1);
     static_assert(O == 27, "the state is read as broadcasts 0 .. 6 of one float4");
     const float4 sv = *reinterpret_cast<const float4*>(&s_state[cur][4 * (o & 7)]);
     const float z1 = dot4_bcast27(w1, sv) + b1v;
@@ -298,13 +353,13 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
       pa = pa + row_shl<4>(pa);   // slices s and s + 4 (groups of 8 never straddle a row)
       pa = pa + row_shl<2>(pa);   // then s + 2
       pa = pa + row_shl<1>(pa);   // then s + 1
-      if (slice == 0) s_a[o3] = tanh32(pa + b3v);
+      if (slice == 0) s_ra[slot][o3] = tanh32(pa + b3v);
     }
     __syncthreads();
     if (o < O) {
       float ba = 0.0f;
 #pragma unroll
-      for (int k = 0; k < A; ++k) ba = fma32(brow[k], s_a[k], ba);
+      for (int k = 0; k < A; ++k) ba = fma32(brow[k], s_ra[slot][k], ba);
       const float sn = tanh32(as + ba);
       s_state[cur ^ 1][o] = sn;
       // lane 0 holds component 0 of the new state (lanes 0..26 share wave 0)
@@ -313,30 +368,29 @@ __global__ __launch_bounds__(H) void k_rollout(const Params p, uint32_t g) {
                             p.death_below;
       if (fail) {
         if (o == 0) s_fail = 1;
-      } else if (o == 0) {
-        float qa = 0.0f;
-#pragma unroll
-        for (int k = 0; k < A; ++k) qa = fma32(s_a[k], s_a[k], qa);
-        ret = ret + fma32(-0.5f, qa, sn);
       } else if (o <= 4) {
-        dsum = dsum + sigmoid32(sn);
+        s_rs[o][slot] = sn;
       }
     }
     cur ^= 1;
     __syncthreads();
     if (s_fail) break;   // the same value in every thread after the barrier
     ++valid;
+    // a full ring: wave 0 folds it in; the other wave cannot write the ring
+    // again before wave 0 has passed the next two barriers
+    if ((valid & (kRing - 1)) == 0 && o < 64) flush_ring<A>(s_ra, s_rs, kRing, o, acc);
   }
+  if (o < 64) flush_ring<A>(s_ra, s_rs, valid & (kRing - 1), o, acc);
   // death flag (Appendix A.4 i): a NaN objective is never inserted
   const bool dead = (p.death_mode == 2 && s_fail) || valid == 0;
   if (o == 0) {
-    p.off_fit[j] = dead ? __builtin_nanf("") : ret;
+    p.off_fit[j] = dead ? __builtin_nanf("") : acc;
     p.off_par[2 * j] = q.c1;
     p.off_par[2 * j + 1] = q.c2;
     p.off_bank[j] = (uint8_t)q.banks;
     p.off_won[j] = 0;
   } else if (o <= 4) {
-    p.off_desc[(size_t)j * 4 + (o - 1)] = valid > 0 ? dsum / (float)valid : 0.0f;
+    p.off_desc[(size_t)j * 4 + (o - 1)] = valid > 0 ? acc / (float)valid : 0.0f;
   }
 }
 
