@@ -20,6 +20,11 @@ import sqlite3
 TRAFFIC_TAG = "traffic_bytes_per_launch"
 
 
+def _open(db_path: str) -> sqlite3.Connection:
+    """A results database, read-only (no journal or lock files are created)."""
+    return sqlite3.connect(f"file:{os.path.abspath(db_path)}?mode=ro&immutable=1", uri=True)
+
+
 # Sources a kernel's code depends on: every kernel is built from the device
 # helpers, the kernel header, the launch code and the build flags; the policy
 # kernels also from the rollout header.
@@ -59,7 +64,7 @@ def recorded_traffic(summary_path: str, kernel: str) -> float | None:
 
 
 def summary(db_path: str, top: int = 20) -> str:
-    con = sqlite3.connect(db_path)
+    con = _open(db_path)
     rows = con.execute(
         "select name, count(*), sum(end - start), avg(end - start), min(end - start), "
         "max(end - start) from kernels group by name order by sum(end - start) desc").fetchall()
@@ -73,7 +78,7 @@ def summary(db_path: str, top: int = 20) -> str:
 
 
 def pmc_summary(db_path: str, top: int = 20) -> str:
-    con = sqlite3.connect(db_path)
+    con = _open(db_path)
     rows = con.execute(
         "select name, counter_name, count(*), avg(counter_value), min(counter_value), "
         "max(counter_value) from pmc_events group by name, counter_name "
@@ -86,7 +91,7 @@ def pmc_summary(db_path: str, top: int = 20) -> str:
 
 
 def _counter_mean(db_path: str, counter: str, name_like: str) -> tuple[float, int]:
-    con = sqlite3.connect(db_path)
+    con = _open(db_path)
     row = con.execute("select avg(counter_value), count(*) from pmc_events where counter_name = ? "
                       "and name like ?", (counter, name_like)).fetchone()
     if row is None or row[1] == 0:
