@@ -174,6 +174,14 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
  * nothing. */
 qd_status qd_generation(qd_archive* h, uint32_t gen_index, void* stream);
 
+/* Enqueues generations first_gen, first_gen + 1, ..., first_gen + count - 1
+ * on `stream`, in order: the same work as that many qd_generation() calls,
+ * without a return to the caller between them (Algorithm 1's loop).  count 0
+ * enqueues nothing.  QD_ERR_INVALID_ARG for a null handle, first_gen 0 or a
+ * last index beyond 2^32 - 1, before any launch; a launch failure stops the
+ * run and returns QD_ERR_HIP.  Asynchronous, like qd_generation(). */
+qd_status qd_generations(qd_archive* h, uint32_t first_gen, uint32_t count, void* stream);
+
 /* QD-score (Eq. 1) with each filled cell's objective shifted by qd_offset,
  * coverage and best objective (Appendix B.1), computed on the device and
  * copied into *out.  Synchronises `stream` (the only call that does). */

@@ -404,6 +404,15 @@ qd_status qd_generation(qd_archive* h, uint32_t gen_index, void* stream) {
   return enqueue_generation<false>(h, (hipStream_t)stream, gen_index);
 }
 
+qd_status qd_generations(qd_archive* h, uint32_t first_gen, uint32_t count, void* stream) {
+  if (!h || first_gen == 0 || (uint64_t)first_gen + count - 1 > UINT32_MAX) return QD_ERR_INVALID_ARG;
+  for (uint32_t k = 0; k < count; ++k) {
+    const qd_status st = enqueue_generation<false>(h, (hipStream_t)stream, first_gen + k);
+    if (st != QD_OK) return st;
+  }
+  return QD_OK;
+}
+
 qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_stats* out) {
   if (!h || !out) return QD_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;

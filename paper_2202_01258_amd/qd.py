@@ -30,7 +30,8 @@ QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
 KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
 
 # Every symbol include/qd.h declares.
-EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_archive_stats",
+EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_generations",
+           "qd_archive_stats",
            "qd_archive_layout", "qd_set_kernel_timing", "qd_kernel_times",
            "qd_check_fast_arith", "qd_archive_destroy", "qd_status_str"]
 
@@ -87,6 +88,7 @@ def lib():
         L.qd_layout_query.argtypes = [C.POINTER(QdConfig), C.POINTER(QdLayout)]
         L.qd_archive_init.argtypes = [C.POINTER(QdConfig), P, C.c_uint64, P, C.POINTER(P)]
         L.qd_generation.argtypes = [P, C.c_uint32, P]
+        L.qd_generations.argtypes = [P, C.c_uint32, C.c_uint32, P]
         L.qd_archive_stats.argtypes = [P, C.c_double, P, C.POINTER(QdStats)]
         L.qd_archive_layout.argtypes = [P, C.POINTER(QdLayout)]
         L.qd_set_kernel_timing.argtypes = [P, C.c_uint32]
@@ -196,6 +198,11 @@ class Archive:
     def generation(self, g: int):
         _check(lib().qd_generation(self._h, g, C.c_void_p(_stream_handle(self.stream))),
                "qd_generation")
+
+    def generations(self, first: int, count: int):
+        """Generations first .. first + count - 1, enqueued by one library call."""
+        _check(lib().qd_generations(self._h, first, count,
+                                    C.c_void_p(_stream_handle(self.stream))), "qd_generations")
 
     def stats(self, offset: float = 0.0) -> dict:
         out = QdStats()

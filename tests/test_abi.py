@@ -149,6 +149,10 @@ def test_workspace_checks_happen_before_gpu_work(lib):
     st = lib.qd_archive_init(C.byref(c), None, lay.workspace_bytes, None, C.byref(h))
     assert st == Q.QD_ERR_INVALID_ARG
     assert lib.qd_generation(None, 1, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_generations(None, 1, 4, None) == Q.QD_ERR_INVALID_ARG
+    # argument checks come before the handle is used
+    assert lib.qd_generations(fake, 0, 4, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_generations(fake, 0xFFFFFFFF, 2, None) == Q.QD_ERR_INVALID_ARG
     assert lib.qd_archive_destroy(None) == Q.QD_OK
     assert Q.status_str(Q.QD_ERR_WORKSPACE_TOO_SMALL) == "workspace too small"
 

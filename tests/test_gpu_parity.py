@@ -227,6 +227,27 @@ def test_replay_is_deterministic():
         np.testing.assert_array_equal(a.snapshot()[k], b.snapshot()[k])
 
 
+@pytest.mark.parametrize("name,kw", [("sphere_grid_b16384", dict(batch=3000)),
+                                     ("mlp64_cvt_b8192", dict(batch=24, T=20))])
+def test_generations_in_one_call_equal_single_calls(name, kw):
+    """qd_generations(first, count) leaves the archive and the last batch
+    exactly as count qd_generation() calls do."""
+    w = W.workload(name, **kw)
+    say(f"generations in one call: {name} {kw}")
+    a = qd().Archive(w, keep_offspring=True)
+    for g in range(1, 6):
+        a.generation(g)
+    b = qd().Archive(w, keep_offspring=True)
+    b.generations(1, 5)
+    b.generations(6, 0)                  # count 0: nothing
+    sa, sb = a.snapshot(), b.snapshot()
+    for k in ("key", "fit", "desc", "geno", "occ_list"):
+        np.testing.assert_array_equal(sa[k], sb[k], err_msg=k)
+    la, lb = a.last_batch(), b.last_batch()
+    for k in ("geno", "fit", "desc", "cell", "won"):
+        np.testing.assert_array_equal(la[k], lb[k], err_msg=k)
+
+
 @pytest.mark.parametrize("batch", [65536, 131072])
 def test_full_size_rastrigin_projection_sampled(batch):
     """n = 1000, CVT 10^4 at N_B = 65536 (the benchmark's launch configuration)
