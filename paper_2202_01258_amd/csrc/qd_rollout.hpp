@@ -204,7 +204,7 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 // Folds the first m ring slots into the running sums; called by all 64
-// lanes of wave 0.  Lane i < m turns slot i into its step's reward
+// lanes of the output wave (o: lane index in it).  Lane i < m turns slot i into its step's reward
 // s'_0 - 0.5 |a|^2 (|a|^2 as an fma chain over the actions in order) and the
 // sigmoids of s'_1 .. s'_4; then lane 0 adds the m rewards and lanes 1 .. 4
 // their m sigmoids to `acc`, in slot (= step) order -- the same operations in
@@ -239,17 +239,17 @@ __device__ __forceinline__ void flush_ring(float (*ra)[A], float (*rs)[kRing + 1
 
 // One individual per workgroup of H threads (H / 64 waves):
 //   thread o      row o of W1 and W2, b1[o], b2[o] in VGPRs; hidden neuron o
-//   thread i < 27 row i of A and B (shared environment) in VGPRs; state i
-//   output wave   64 lanes (o3 = lane / 8, slice = lane % 8) hold W3[o3][slice
-//                 of H/8 inputs]; the 8 partial sums of an action are folded
-//                 inside its group of 8 lanes.  With H = 128 this is the second
-//                 wave, so the output layer and the dynamics run on different
-//                 waves.
-// Per step: layer 1 and the A s product, layer 2, output layer, B a product
-// and the new state; activations pass through LDS with one barrier per stage.
-// The reward and the descriptor's sigmoids, which only lanes 0 .. 4 need,
-// are not evaluated in the step: the step's actions and new-state components
-// 0 .. 4 go to a ring in LDS, folded in every kRing steps by all of wave 0.
+//   output wave   the last wave.  Its 64 lanes (o3 = lane / 8, slice = lane %
+//                 8) hold W3[o3][slice of H/8 inputs]; the 8 partial sums of an
+//                 action are folded inside its group of 8 lanes.  Its lanes
+//                 i < 27 also hold row i of A and B (shared environment) and
+//                 compute state component i.
+// Per step: layer 1 (and A s on the output wave), barrier, layer 2, barrier,
+// then on the output wave alone the output layer, B a (the actions broadcast
+// by readlane) and the new state, barrier.  The reward and the descriptor's
+// sigmoids, which only lanes 0 .. 4 of the output wave need, are not
+// evaluated in the step: the step's actions and new-state components 0 .. 4
+// go to a ring in LDS, folded in every kRing steps by the output wave.
 template <int H, bool GEN0, bool KEEP>
 __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, uint32_t g) {
   constexpr int O = kObs, A = kAct, SL = H / 8;
@@ -285,6 +285,7 @@ __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, 
   // ---- prologue: this individual's genotype, straight into registers
   const bool out_lane = o >= OUT_WAVE_FIRST;
   const int ol = o - OUT_WAVE_FIRST, o3 = (ol >> 3) & 7, slice = ol & 7;
+  const bool dyn_lane = out_lane && ol < O;   // holds state component ol
   float w1[O], w2[H], w3[SL], arow[O], brow[A];
   float b1v, b2v, b3v = 0.0f;
   mlp_genes_run<GEN0, O>(p, q, g, j, o * O, w1);
@@ -317,21 +318,21 @@ __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, 
   const float* envS = p.env + O * O + O * A;
 #pragma unroll
   for (int k = 0; k < O; ++k) arow[k] = 0.0f;
-  if (o < O) {
+  if (dyn_lane) {
 #pragma unroll
-    for (int k = 0; k < O; ++k) arow[k] = envA[o * O + k];
+    for (int k = 0; k < O; ++k) arow[k] = envA[ol * O + k];
 #pragma unroll
-    for (int k = 0; k < A; ++k) brow[k] = envB[o * A + k];
-    s_state[0][o] = envS[o];
+    for (int k = 0; k < A; ++k) brow[k] = envB[ol * A + k];
+    s_state[0][ol] = envS[ol];
   }
   if (o == 0) s_fail = 0;
   __syncthreads();
 
   // ---- episode; with death_mode != 0 it ends at the first new state whose
   // component 0 is below death_below, and that step counts for nothing.
-  // Lane 0 sums the rewards, lanes 1 .. 4 the sigmoids of state components
-  // 1 .. 4, each in step order; both are worked out from the ring, kRing
-  // steps at a time (flush_ring), not inside the step.
+  // Output-wave lane 0 sums the rewards, lanes 1 .. 4 the sigmoids of state
+  // components 1 .. 4, each in step order; both are worked out from the ring,
+  // kRing steps at a time (flush_ring), not inside the step.
   float acc = 0.0f;
   int cur = 0, valid = 0;
   for (int step = 0; step < p.T; ++step) {
@@ -340,7 +341,7 @@ __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, 
     const float4 sv = *reinterpret_cast<const float4*>(&s_state[cur][4 * (o & 7)]);
     const float z1 = dot4_bcast27(w1, sv) + b1v;
     float as = 0.0f;
-    if (o < 64) as = dot4_bcast27(arow, sv);   // all of wave 0 (lanes 0 .. O-1 use it)
+    if (out_lane) as = dot4_bcast27(arow, sv);   // the whole output wave (dyn_lane uses it)
     s_h1[o] = tanh32(z1);
     __syncthreads();
     const float z2 = dot4_bcast<H>(w2, s_h1) + b2v;
@@ -353,44 +354,47 @@ __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, 
       pa = pa + row_shl<4>(pa);   // slices s and s + 4 (groups of 8 never straddle a row)
       pa = pa + row_shl<2>(pa);   // then s + 2
       pa = pa + row_shl<1>(pa);   // then s + 1
-      if (slice == 0) s_ra[slot][o3] = tanh32(pa + b3v);
-    }
-    __syncthreads();
-    if (o < O) {
-      float ba = 0.0f;
+      const float act = tanh32(pa + b3v);   // action o3 in lane 8 o3 (slice 0)
+      if (slice == 0) s_ra[slot][o3] = act;
+      float ak[A];
 #pragma unroll
-      for (int k = 0; k < A; ++k) ba = fma32(brow[k], s_ra[slot][k], ba);
-      const float sn = tanh32(as + ba);
-      s_state[cur ^ 1][o] = sn;
-      // lane 0 holds component 0 of the new state (lanes 0..26 share wave 0)
-      const bool fail = p.death_mode != 0 &&
-                        __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(sn), 0)) <
-                            p.death_below;
-      if (fail) {
-        if (o == 0) s_fail = 1;
-      } else if (o <= 4) {
-        s_rs[o][slot] = sn;
+      for (int k = 0; k < A; ++k)
+        ak[k] = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(act), 8 * k));
+      if (dyn_lane) {
+        float ba = 0.0f;
+#pragma unroll
+        for (int k = 0; k < A; ++k) ba = fma32(brow[k], ak[k], ba);
+        const float sn = tanh32(as + ba);
+        s_state[cur ^ 1][ol] = sn;
+        // lane 0 of this wave holds component 0 of the new state
+        const bool fail = p.death_mode != 0 &&
+                          __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(sn), 0)) <
+                              p.death_below;
+        if (fail) {
+          if (ol == 0) s_fail = 1;
+        } else if (ol <= 4) {
+          s_rs[ol][slot] = sn;
+        }
       }
     }
     cur ^= 1;
     __syncthreads();
     if (s_fail) break;   // the same value in every thread after the barrier
     ++valid;
-    // a full ring: wave 0 folds it in; the other wave cannot write the ring
-    // again before wave 0 has passed the next two barriers
-    if ((valid & (kRing - 1)) == 0 && o < 64) flush_ring<A>(s_ra, s_rs, kRing, o, acc);
+    // a full ring: the output wave, its only writer, folds it in
+    if ((valid & (kRing - 1)) == 0 && out_lane) flush_ring<A>(s_ra, s_rs, kRing, ol, acc);
   }
-  if (o < 64) flush_ring<A>(s_ra, s_rs, valid & (kRing - 1), o, acc);
+  if (out_lane) flush_ring<A>(s_ra, s_rs, valid & (kRing - 1), ol, acc);
   // death flag (Appendix A.4 i): a NaN objective is never inserted
   const bool dead = (p.death_mode == 2 && s_fail) || valid == 0;
-  if (o == 0) {
+  if (out_lane && ol == 0) {
     p.off_fit[j] = dead ? __builtin_nanf("") : acc;
     p.off_par[2 * j] = q.c1;
     p.off_par[2 * j + 1] = q.c2;
     p.off_bank[j] = (uint8_t)q.banks;
     p.off_won[j] = 0;
-  } else if (o <= 4) {
-    p.off_desc[(size_t)j * 4 + (o - 1)] = valid > 0 ? acc / (float)valid : 0.0f;
+  } else if (out_lane && ol <= 4) {
+    p.off_desc[(size_t)j * 4 + (ol - 1)] = valid > 0 ? acc / (float)valid : 0.0f;
   }
 }
 
