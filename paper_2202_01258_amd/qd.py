@@ -141,13 +141,15 @@ def layout_query(cfg: QdConfig) -> QdLayout:
 
 def check_fast_arith(device: str = "cuda:0") -> list:
     """Mismatch counts of the short division / square-root sequences against
-    IEEE arithmetic: [radius (2^24 inputs), tanh (2^32), sigmoid (|x| <= 1)]."""
+    IEEE arithmetic: [Box-Muller radius (all 2^24 inputs), tanh (all 2^32),
+    sigmoid (|x| <= 1)], run on `device` and its current stream."""
     import torch
-    scratch = torch.zeros(3, dtype=torch.int64, device=device)
-    out = (C.c_uint64 * 3)()
-    _check(lib().qd_check_fast_arith(C.c_void_p(scratch.data_ptr()),
-                                     C.c_void_p(_stream_handle(None)), out),
-           "qd_check_fast_arith")
+    with torch.cuda.device(torch.device(device)):
+        scratch = torch.zeros(3, dtype=torch.int64, device=device)
+        out = (C.c_uint64 * 3)()
+        _check(lib().qd_check_fast_arith(C.c_void_p(scratch.data_ptr()),
+                                         C.c_void_p(_stream_handle(None)), out),
+               "qd_check_fast_arith")
     return [int(v) for v in out]
 
 
