@@ -609,6 +609,113 @@ __global__ __launch_bounds__(kInsertBlock) void k_insert(const Params p) {
   }
 }
 
+// Insertion on a four-dimensional CVT small enough for LDS (C <= kCvtLdsCells):
+// the workgroup stages every centroid in LDS and takes kInsertLdsOffspring
+// offspring, four per wave, 16 lanes per offspring.  Lane s of a row
+// measures centroids s, s + 16, ... (the same fma chain as the ring search,
+// keeping the first smallest), then the row keeps its smallest (distance,
+// index) pair -- the brute-force argmin with ties to the lower index.  Wave 0
+// then packs the keys and folds them per cell before the global atomicMax.
+constexpr int kCvtLdsCells = 2048, kInsertLdsOffspring = 16;
+
+// Squared distance from u to centroid c: fma chain over the dimensions.
+__device__ __forceinline__ float cvt_dist4(const float* u, const float4& c) {
+  const float cc[4] = {c.x, c.y, c.z, c.w};
+  float acc = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float diff = u[k] - cc[k];
+    acc = fma32(diff, diff, acc);
+  }
+  return acc;
+}
+
+__global__ __launch_bounds__(256) void k_insert_cvt_lds(const Params p) {
+  constexpr int D = 4;
+  __shared__ float4 s_cent[kCvtLdsCells];
+  __shared__ int s_cell[kInsertLdsOffspring];
+  const float4* cent = reinterpret_cast<const float4*>(p.cent);
+  for (int i = threadIdx.x; i < p.C; i += 256) s_cent[i] = cent[i];
+  __syncthreads();
+  const int lane = lane_id(), wave = threadIdx.x >> 6, row = lane >> 4, sub = lane & 15;
+  const int first = blockIdx.x * kInsertLdsOffspring;
+#pragma unroll 1
+  for (int r = 0; r < kInsertLdsOffspring / 16; ++r) {
+    const int t = r * 16 + wave * 4 + row;
+    const int j = first + t;
+    bool live = false;
+    float u[D];
+    if (j < p.nb && p.off_fit[j] == p.off_fit[j]) {
+      live = true;
+#pragma unroll
+      for (int k = 0; k < D; ++k) {
+        const float d = p.off_desc[(size_t)j * D + k];
+        live = live && d == d;
+        u[k] = (d - p.lo[k]) / p.span[k];
+      }
+    }
+    float best = __builtin_inff();
+    int best_idx = 0x7fffffff;
+    if (live) {
+      int i = sub;
+      for (; i + 48 < p.C; i += 64) {   // four loads in flight, compared in index order
+        float4 c4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) c4[q] = s_cent[i + 16 * q];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float acc = cvt_dist4(u, c4[q]);
+          // (distance, index) order, as the ring search: an infinite distance
+          // still names a centroid, so a live row always gets a cell < C
+          if (acc < best || (acc == best && i + 16 * q < best_idx)) {
+            best = acc;
+            best_idx = i + 16 * q;
+          }
+        }
+      }
+      for (; i < p.C; i += 16) {
+        const float acc = cvt_dist4(u, s_cent[i]);
+        if (acc < best || (acc == best && i < best_idx)) {
+          best = acc;
+          best_idx = i;
+        }
+      }
+    }
+    min_pair_row<8>(best, best_idx);
+    min_pair_row<4>(best, best_idx);
+    min_pair_row<2>(best, best_idx);
+    min_pair_row<1>(best, best_idx);
+    if (sub == 0) s_cell[t] = live ? best_idx : -1;
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  // lanes 0 .. kInsertLdsOffspring - 1 of wave 0 take this workgroup's offspring
+  static_assert(kInsertLdsOffspring % 16 == 0 && kInsertLdsOffspring <= 64, "one wave folds them");
+  const int j = first + lane;
+  int cell = -1;
+  uint64_t key = 0ull;
+  if (lane < kInsertLdsOffspring && j < p.nb) {
+    cell = s_cell[lane];
+    key = insert_key(p, p.off_fit[j], cell, j);
+    p.off_cell[j] = cell;
+    p.off_key[j] = key;
+  }
+  uint64_t todo = __ballot(cell >= 0);
+  while (todo) {
+    const int leader = __ffsll((unsigned long long)todo) - 1;
+    const int c = __shfl(cell, leader, 64);
+    const uint64_t same = __ballot(cell == c);
+    uint64_t k = cell == c ? key : 0ull;
+#pragma unroll
+    for (int h = 32; h >= 1; h >>= 1) {
+      const uint64_t o = __shfl_xor(k, h, 64);
+      k = o > k ? o : k;
+    }
+    if (lane == leader) insert_one(p, c, k);
+    todo &= ~same;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Compaction of the filled cells into the ascending list the next selection
 // draws from (Appendix A.2).  Run by one extra workgroup of the winner kernel,

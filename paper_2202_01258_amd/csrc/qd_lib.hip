@@ -241,6 +241,8 @@ void launch_insert(qd_archive* h, hipStream_t s) {
   if (p.tess == qd::kTessGrid) {
     if (p.D == 2) go(qd::k_insert<qd::kTessGrid, 2>, grid, block, p);
     else go(qd::k_insert<qd::kTessGrid, 4>, grid, block, p);
+  } else if (p.D == 4 && p.C <= qd::kCvtLdsCells) {
+    go(qd::k_insert_cvt_lds, dim3(blocks_for((uint64_t)p.nb, qd::kInsertLdsOffspring)), dim3(256), p);
   } else {
     if (p.D == 2) go(qd::k_insert<qd::kTessCvt, 2>, grid, block, p);
     else go(qd::k_insert<qd::kTessCvt, 4>, grid, block, p);
