@@ -61,23 +61,10 @@ __device__ __forceinline__ void settle(float4& v) {
   __asm__ volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
 }
 
-// Dot product in four interleaved partial sums (input k -> partial k mod 4,
-// each an fma chain in input order), folded as (p0 + p2) + (p1 + p3): four
-// independent dependency chains per lane.
-template <int N>
-__device__ __forceinline__ float dot4(const float* w, const float* x) {
-  float p0 = 0.0f, p1 = 0.0f, p2 = 0.0f, p3 = 0.0f;
-#pragma unroll
-  for (int k = 0; k < N; k += 4) {
-    p0 = fma32(w[k], x[k], p0);
-    if (k + 1 < N) p1 = fma32(w[k + 1], x[k + 1], p1);
-    if (k + 2 < N) p2 = fma32(w[k + 2], x[k + 2], p2);
-    if (k + 3 < N) p3 = fma32(w[k + 3], x[k + 3], p3);
-  }
-  return (p0 + p2) + (p1 + p3);
-}
-
-// The same sums with the inputs broadcast from registers instead of LDS.
+// The layers' dot products: four interleaved partial sums (input k goes to
+// partial k mod 4, each an fma chain in input order from 0), folded as
+// (p0 + p2) + (p1 + p3) -- four independent dependency chains per lane.  The
+// inputs are broadcast from registers, not read from LDS one by one.
 // With the DPP control row_newbcast:m, the first source of v_fmac_f32 is
 // read from lane m of the executing lane's row of 16.  Component t of `v`
 // holds, in lane 16 r + m, input 4 m + t of a run of 64 inputs (the same in
@@ -130,7 +117,7 @@ __device__ __forceinline__ void bfma11(float (&acc)[4], const float4& v, const f
               QD_BROW3(6, 16, 17, 18) QD_BFMA_IO(w));
 }
 
-// dot4<N> for N a multiple of 64; run r of x is read as one float4 per lane
+// That dot product for N a multiple of 64; run r of x is read as one float4 per lane
 // from x + 64 r + 4 (lane mod 16), 16-byte aligned.
 template <int N>
 __device__ __forceinline__ float dot4_bcast(const float* w, const float* x) {
@@ -148,7 +135,7 @@ __device__ __forceinline__ float dot4_bcast(const float* w, const float* x) {
   return (acc[0] + acc[2]) + (acc[1] + acc[3]);
 }
 
-// dot4<27> on `v`, the float4 a lane reads from x + 4 (lane mod 8) of a
+// That dot product for N = 27 on `v`, the float4 a lane reads from x + 4 (lane mod 8) of a
 // 32-float, 16-byte aligned x (its input 27 and broadcast 7 are never used).
 __device__ __forceinline__ float dot4_bcast27(const float* w, const float4& v) {
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -204,11 +191,12 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 // Folds the first m ring slots into the running sums; called by all 64
-// lanes of the output wave (o: lane index in it).  Lane i < m turns slot i into its step's reward
-// s'_0 - 0.5 |a|^2 (|a|^2 as an fma chain over the actions in order) and the
-// sigmoids of s'_1 .. s'_4; then lane 0 adds the m rewards and lanes 1 .. 4
-// their m sigmoids to `acc`, in slot (= step) order -- the same operations in
-// the same order as adding each step's terms as the step ends.
+// lanes of the output wave (o: lane index in it).  Lane i < m turns slot i
+// into its step's reward s'_0 - 0.5 |a|^2 (|a|^2 as an fma chain over the
+// actions in order) and the sigmoids of s'_1 .. s'_4; then lane 0 adds the m
+// rewards and lanes 1 .. 4 their m sigmoids to `acc`, in slot (= step) order
+// -- the same operations in the same order as adding each step's terms as
+// the step ends.
 template <int A>
 __device__ __forceinline__ void flush_ring(float (*ra)[A], float (*rs)[kRing + 1], int m, int o,
                                            float& acc) {
