@@ -132,8 +132,11 @@ __device__ __forceinline__ float4 make_genes(const Params& p, const Pair& q, uin
                        fma32(unit24(x.z), p.init_span, p.init_lo),
                        fma32(unit24(x.w), p.init_span, p.init_lo));
   } else {
-    const float4 t1 = *reinterpret_cast<const float4*>(q.row1 + base);
-    const float4 t2 = *reinterpret_cast<const float4*>(q.row2 + base);
+    // wave-uniform row pointer + 32-bit unsigned byte offset (rows are far
+    // below 4 GiB): the address form of a scalar base and a vector offset
+    const uint32_t off = 4u * (uint32_t)base;
+    const float4 t1 = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(q.row1) + off);
+    const float4 t2 = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(q.row2) + off);
     const uint4 x = philox((uint32_t)(base >> 2), (uint32_t)j, g, kTagIso, p.key);
     const float2 e01 = gauss2(x.x, x.y, q.tb);
     const float2 e23 = gauss2(x.z, x.w, q.tb);
@@ -452,7 +455,10 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
     float acc = 0.0f, dlo = 0.0f, dhi = 0.0f;
     float g0 = 0.0f, g1 = 0.0f;
     float* keep_row = KEEP ? p.off_geno + (size_t)j * (size_t)p.stride : nullptr;
-    for (int base = 4 * lane; base < n; base += 256) {
+    const int nchunks = (n + 255) >> 8;
+    for (int c = 0; c < nchunks; ++c) {   // a wave-uniform trip count
+      const int base = 256 * c + 4 * lane;
+      if (base >= n) continue;
       const float4 v4 = make_genes<GEN0>(p, q, g, j, base);
       if (KEEP) *reinterpret_cast<float4*>(keep_row + base) = v4;
       if (base == 0) {
