@@ -303,6 +303,10 @@ MLP_SMALL = {
     # a batch that is not a multiple of the 16 offspring an LDS-CVT insertion
     # workgroup takes, on a CVT smaller than one centroid per lane
     "mlp64_odd_batch_small_cvt": ("mlp64_cvt_b8192", dict(batch=37, T=12, C=13)),
+    # the largest CVT whose centroids the insertion stages in LDS, and the
+    # smallest one searched by rings instead
+    "mlp64_cvt_2048_lds": ("mlp64_cvt_b8192", dict(batch=40, T=8, C=2048)),
+    "mlp64_cvt_2049_rings": ("mlp64_cvt_b8192", dict(batch=40, T=8, C=2049)),
 }
 
 
