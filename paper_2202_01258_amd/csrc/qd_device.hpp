@@ -345,6 +345,21 @@ __device__ __forceinline__ float wave_fold_sum(float v) {
   return v;
 }
 
+// wave_fold_sum for partials that are zero in lanes 32 .. 63 of the wave the
+// R64 order describes (at most 128 genes: its h = 32 step adds +0 and changes
+// nothing), with two such waves packed into the two halves of this one: the
+// h = 16 .. 1 steps stay inside each half, whose every lane ends up with its
+// half's sum.
+__device__ __forceinline__ float half_fold_sum(float v) {
+  const auto h16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(h16[0]) + __uint_as_float(h16[1]);
+  v = v + row_ror<8>(v);
+  v = v + row_ror<4>(v);
+  v = v + row_ror<2>(v);
+  v = v + row_ror<1>(v);
+  return v;
+}
+
 // The same fold for three values at once.  The first two steps pack values
 // into halves and rows of one register (a half-swap of a with b leaves lane l
 // of the sum holding a_l + a_{l+32} below lane 32 and b's pair sums above;

@@ -440,6 +440,61 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   const int n = p.n;
   const int half = n >> 1;
   float my_f = 0.0f, my_d0 = 0.0f, my_d1 = 0.0f;
+  if (TASK != kTaskProj && n <= 128) {
+    // Short genotypes: two offspring at a time, one per 32-lane half (lane h
+    // of a half owns genes 4h .. 4h + 3, as lane h of a whole wave would, and
+    // the fold stays in the half).  With an odd count the spare half repeats
+    // its partner and its result is dropped.
+    const int hl = lane >> 5, hlane = lane & 31;
+    for (int i = 0; i < nmine; i += 2) {
+      const int ib = i + 1 < nmine ? i + 1 : i;   // the upper half's offspring slot
+      const int j = j0 + (hl ? ib : i);
+      Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u, tb};
+      if (!GEN0) {
+        const int c1a = __builtin_amdgcn_readlane(sel.c1, i), c1b = __builtin_amdgcn_readlane(sel.c1, ib);
+        const int c2a = __builtin_amdgcn_readlane(sel.c2, i), c2b = __builtin_amdgcn_readlane(sel.c2, ib);
+        const int bka = __builtin_amdgcn_readlane((int)sel.banks, i);
+        const int bkb = __builtin_amdgcn_readlane((int)sel.banks, ib);
+        const uint32_t lma = __builtin_amdgcn_readlane(__float_as_uint(sel.lambda), i);
+        const uint32_t lmb = __builtin_amdgcn_readlane(__float_as_uint(sel.lambda), ib);
+        q.c1 = hl ? c1b : c1a;
+        q.c2 = hl ? c2b : c2a;
+        q.banks = (uint32_t)(hl ? bkb : bka);
+        q.lambda = __uint_as_float(hl ? lmb : lma);
+        q.row1 = geno_row(p, q.banks & 1u, q.c1);
+        q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
+      }
+      const int base = 4 * hlane;
+      float acc = 0.0f, g0 = 0.0f, g1 = 0.0f;
+      if (base < n) {
+        const float4 v4 = make_genes<GEN0>(p, q, g, j, base);
+        if (KEEP && (hl == 0 || ib != i))
+          *reinterpret_cast<float4*>(p.off_geno + (size_t)j * (size_t)p.stride + base) = v4;
+        g0 = v4.x;
+        g1 = v4.y;
+        const float v[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (base + k < n) acc = acc + task_term<TASK>(v[k]);
+      }
+      const float f = half_fold_sum(acc);
+      const float fa = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(f), 0));
+      const float fb = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(f), 32));
+      const float g0a = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g0), 0));
+      const float g1a = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g1), 0));
+      const float g0b = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g0), 32));
+      const float g1b = __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(g1), 32));
+      if (lane == i) {
+        my_f = -fa;
+        my_d0 = clip(g0a, p.lo[0], p.hi[0]);
+        my_d1 = clip(g1a, p.lo[1], p.hi[1]);
+      } else if (lane == ib) {
+        my_f = -fb;
+        my_d0 = clip(g0b, p.lo[0], p.hi[0]);
+        my_d1 = clip(g1b, p.lo[1], p.hi[1]);
+      }
+    }
+  } else
   for (int i = 0; i < nmine; ++i) {
     const int j = j0 + i;
     Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u, tb};
