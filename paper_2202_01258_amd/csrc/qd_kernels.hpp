@@ -2,17 +2,20 @@
 //
 // Pipeline of one generation (Algorithm 1 after the first iteration; the
 // first iteration runs the same kernels with the random-init genotype):
-//   k_vary_eval   a wave takes 4 offspring: draws their parents uniformly from
-//                 the filled cells (Appendix A.2), runs Iso+LineDD (Algorithm
-//                 2) gene by gene on coalesced float4 rows of both parents with
+//   k_vary_eval   a wave takes 4 offspring (two at a time, one per half-wave,
+//                 for genotypes of at most 128 genes): draws their parents
+//                 uniformly from the filled cells (Appendix A.2), runs Iso+LineDD
+//                 (Algorithm 2) gene by gene on coalesced float4 rows of both parents with
 //                 the objective / descriptor reduction (Appendix B.2) in the
 //                 same pass, then finds each offspring's cell (grid bin, or
 //                 exact nearest CVT centroid through a bucket grid) and inserts
 //                 its packed key with a 64-bit atomicMax that only offspring
 //                 beating the cell's current key issue.  Offspring genotypes
 //                 are not stored.
-//   k_rollout     (policies, qd_rollout.hpp) then k_insert: the same outputs;
-//                 keys folded per wave and per workgroup before the atomics.
+//   k_rollout     (policies, qd_rollout.hpp) then k_insert_cvt_lds (a 4-D
+//                 CVT of at most 2048 cells, searched from LDS) or k_insert:
+//                 the same outputs; keys folded per wave (and per workgroup)
+//                 before the atomics.
 //   k_regen       a workgroup per few cells: a cell whose key now names an
 //                 offspring regenerates that offspring's genotype into the
 //                 cell's other genotype bank (the parents' banks were recorded
