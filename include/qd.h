@@ -193,7 +193,10 @@ qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
 /* Selects the kernels whose launches carry a pair of HIP events on the launch
  * stream (hipExtLaunchKernelGGL: the runtime stamps them when the dispatch
  * begins and ends): bit k of kernel_mask is kernel QD_K_k (0 = no timing, the
- * default).  QD_ERR_INVALID_ARG for bits beyond QD_NUM_KERNELS. */
+ * default).  The handle keeps every timed launch's events until
+ * qd_kernel_times() collects them (two events per launch), so a caller that
+ * times many launches collects periodically.  QD_ERR_INVALID_ARG for bits
+ * beyond QD_NUM_KERNELS. */
 qd_status qd_set_kernel_timing(qd_archive* h, uint32_t kernel_mask);
 
 /* Waits for the recorded events and returns, per QD_K_* kernel, the summed
