@@ -33,9 +33,40 @@ _COMMON = ["csrc/qd_device.hpp", "csrc/qd_kernels.hpp", "csrc/qd_lib.hip", "buil
 _POLICY = ["csrc/qd_rollout.hpp"]
 
 
+def _code_text(path: str) -> bytes:
+    """A source file's code without comments and whitespace runs (C-family
+    files), so that editing documentation does not void recorded counters;
+    other files as they are."""
+    with open(path, "rb") as fh:
+        text = fh.read()
+    if not path.endswith((".hpp", ".hip", ".h")):
+        return text
+    src = text.decode()
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c == '"' or c == "'":                      # literals are code
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            i = src.find("\n", i)
+            i = n if i < 0 else i
+        elif src.startswith("/*", i):
+            i = src.find("*/", i + 2)
+            i = n if i < 0 else i + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split()).encode()
+
+
 def sources_digest(kernel: str) -> str:
-    """sha256 over the sources `kernel` (a demangled name) is built from, in
-    name order; counters taken on other sources do not describe it."""
+    """sha256 over the code of the sources `kernel` (a demangled name) is
+    built from, in name order; counters taken on other code do not describe
+    it."""
     root = os.path.dirname(os.path.abspath(__file__))
     names = list(_COMMON)
     if kernel.startswith(("k_rollout", "k_regen_mlp")):
@@ -44,8 +75,7 @@ def sources_digest(kernel: str) -> str:
     for rel in sorted(names):
         path = os.path.normpath(os.path.join(root, rel))
         h.update(os.path.basename(path).encode())
-        with open(path, "rb") as fh:
-            h.update(fh.read())
+        h.update(_code_text(path))
     return h.hexdigest()
 
 

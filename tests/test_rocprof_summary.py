@@ -34,3 +34,15 @@ def test_committed_summaries_name_their_kernel():
             tagged = [ln.split(maxsplit=3) for ln in fh if ln.startswith(R.TRAFFIC_TAG)]
         assert len(tagged) == 1, name
         assert name.startswith(tagged[0][3].split("<")[0].strip()), name
+
+
+def test_digest_ignores_comments_and_layout_but_not_code(tmp_path):
+    a = tmp_path / "a.hpp"
+    b = tmp_path / "b.hpp"
+    c = tmp_path / "c.hpp"
+    a.write_text('// note\nint f(int x) { return x + 1; }  /* one */\nconst char* s = "// kept";\n')
+    b.write_text('int f(int x) {\n  return x + 1;   // a different note\n}\nconst char* s = "// kept";\n')
+    c.write_text('int f(int x) { return x + 2; }\nconst char* s = "// kept";\n')
+    assert R._code_text(str(a)) == R._code_text(str(b))
+    assert R._code_text(str(a)) != R._code_text(str(c))
+    assert b'"// kept"' in R._code_text(str(a))
