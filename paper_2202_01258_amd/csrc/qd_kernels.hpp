@@ -1140,32 +1140,67 @@ __global__ void k_bucket_fill(const Params p) {
 // relative margin of 1e-5, far above the fp32 error of the distances the
 // search compares) is never the argmin for a point of the box.  The rest are
 // listed in ascending index; the count keeps counting past QD_CAND_SLOTS.
+// kCandGroup lanes per bucket walk the centroids together, staged in LDS
+// tiles: at step i lane q of the group takes centroid kCandGroup i + q.  The
+// bound is the group's minimum (order-free); the listed centroids are
+// appended in q order at each step, i.e. in ascending index.
+constexpr int kCandTile = 2048, kCandGroup = 16, kCandBuckets = 256 / kCandGroup;
+
 __global__ __launch_bounds__(256) void k_cand_build(const Params p) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= p.cand_buckets) return;
+  constexpr int G = kCandGroup;
+  static_assert(G == 4 || G == 8 || G == 16, "a group is a power of two within a row");
+  __shared__ float2 s_c[kCandTile];
+  const int lane = lane_id(), q = lane & (G - 1);
+  const int b = blockIdx.x * kCandBuckets + (int)(threadIdx.x / G);
+  const bool live = b < p.cand_buckets;
   const int R = p.cand_res;
   const double w = 1.0 / (double)R, pad = 1e-6;
-  const double lo0 = (b / R) * w - pad, hi0 = (b / R + 1) * w + pad;
-  const double lo1 = (b % R) * w - pad, hi1 = (b % R + 1) * w + pad;
+  const int bb = live ? b : 0;
+  const double lo0 = (bb / R) * w - pad, hi0 = (bb / R + 1) * w + pad;
+  const double lo1 = (bb % R) * w - pad, hi1 = (bb % R + 1) * w + pad;
+  const float2* cent = reinterpret_cast<const float2*>(p.cent);
   double dmax = __builtin_inf();
-  for (int c = 0; c < p.C; ++c) {
-    const double x = p.cent[2 * c], y = p.cent[2 * c + 1];
-    const double fx = fmax(x - lo0, hi0 - x), fy = fmax(y - lo1, hi1 - y);
-    dmax = fmin(dmax, fx * fx + fy * fy);
-  }
-  const double limit = dmax * (1.0 + 1e-5) + 1e-12;
-  int count = 0;
-  float4* out = p.cand_pts + (size_t)b * QD_CAND_SLOTS;
-  for (int c = 0; c < p.C; ++c) {
-    const double x = p.cent[2 * c], y = p.cent[2 * c + 1];
-    const double gx = fmax(0.0, fmax(lo0 - x, x - hi0)), gy = fmax(0.0, fmax(lo1 - y, y - hi1));
-    if (gx * gx + gy * gy <= limit) {
-      if (count < QD_CAND_SLOTS)
-        out[count] = make_float4(p.cent[2 * c], p.cent[2 * c + 1], __int_as_float(c), 0.0f);
-      ++count;
+  for (int t0 = 0; t0 < p.C; t0 += kCandTile) {
+    const int tn = p.C - t0 < kCandTile ? p.C - t0 : kCandTile;
+    __syncthreads();
+    for (int e = threadIdx.x; e < tn; e += 256) s_c[e] = cent[t0 + e];
+    __syncthreads();
+    for (int e = q; e < tn; e += G) {
+      const double x = s_c[e].x, y = s_c[e].y;
+      const double fx = fmax(x - lo0, hi0 - x), fy = fmax(y - lo1, hi1 - y);
+      dmax = fmin(dmax, fx * fx + fy * fy);
     }
   }
-  p.cand_count[b] = count;
+#pragma unroll
+  for (int h = 1; h < G; h <<= 1) dmax = fmin(dmax, __shfl_xor(dmax, h, 64));   // group minimum
+  const double limit = dmax * (1.0 + 1e-5) + 1e-12;
+  int count = 0;
+  float4* out = p.cand_pts + (size_t)bb * QD_CAND_SLOTS;
+  const int group0 = lane & ~(G - 1);
+  const uint32_t gmask = (uint32_t)((1ull << G) - 1ull);
+  for (int t0 = 0; t0 < p.C; t0 += kCandTile) {
+    const int tn = p.C - t0 < kCandTile ? p.C - t0 : kCandTile;
+    __syncthreads();
+    for (int e = threadIdx.x; e < tn; e += 256) s_c[e] = cent[t0 + e];
+    __syncthreads();
+    for (int e0 = 0; e0 < tn; e0 += G) {   // the group's centroids e0 .. e0 + G - 1
+      const int e = e0 + q;
+      bool hit = false;
+      float2 c = make_float2(0.0f, 0.0f);
+      if (e < tn) {
+        c = s_c[e];
+        const double x = c.x, y = c.y;
+        const double gx = fmax(0.0, fmax(lo0 - x, x - hi0)), gy = fmax(0.0, fmax(lo1 - y, y - hi1));
+        hit = gx * gx + gy * gy <= limit;
+      }
+      const uint32_t bits = (uint32_t)(__ballot(hit) >> group0) & gmask;
+      const int pos = count + __popc(bits & ((1u << q) - 1u));
+      if (live && hit && pos < QD_CAND_SLOTS)
+        out[pos] = make_float4(c.x, c.y, __int_as_float(t0 + e), 0.0f);
+      count += __popc(bits);
+    }
+  }
+  if (live && q == 0) p.cand_count[b] = count;
 }
 
 // Entry e of [A | B | s0] = 0.1 * normal (e mod 4) of block (e/4, 0, 0, ENV).

@@ -385,7 +385,7 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
       go(qd::k_bucket_count, dim3(blocks_for(p.C, 256)), dim3(256), p);
       go(qd::k_bucket_scan, dim3(1), dim3(1024), p);
       go(qd::k_bucket_fill, dim3(blocks_for(p.C, 256)), dim3(256), p);
-      if (p.cand_buckets > 0) go(qd::k_cand_build, dim3(blocks_for(p.cand_buckets, 256)), dim3(256), p);
+      if (p.cand_buckets > 0) go(qd::k_cand_build, dim3(blocks_for(p.cand_buckets, qd::kCandBuckets)), dim3(256), p);
     }
     if (p.task == qd::kTaskMlp) {
       const int count = p.obs * (p.obs + p.act + 1);
