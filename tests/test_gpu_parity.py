@@ -186,7 +186,9 @@ def test_generations_driven_bit_exact(name):
 @pytest.mark.parametrize("name,kw,G", [
     ("rastrigin_grid_b128", {}, 100),                        # the full configuration
     ("sphere_grid_b16384", dict(batch=2048), 40),
+    ("sphere_grid_b16384", {}, 500),                         # the full configuration
     ("rastrigin_proj_cvt_b65536", dict(batch=2048), 12),
+    ("rastrigin_proj_cvt_b65536", {}, 3),                    # the benchmark configuration
 ])
 def test_end_to_end_qd_score(name, kw, G):
     w = W.workload(name, **kw)
