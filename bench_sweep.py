@@ -12,11 +12,13 @@ for N_B = 64, 128, ..., 131072 (doubling),
     I = ceil(H / N_B) iterations, the first one counted (Section 4).
 
 Default workloads: the Rastrigin-projection shape (n = 1000, CVT 10^4) and
-the 27-64-64-8 policy shape (T = 250, CVT 1024).  One GPU.  Prints one JSON
+the 27-64-64-8 policy shape (T = 250, CVT 1024).  One GPU.  With --seeds S
+every (workload, N_B) runs for seeds 0 .. S-1 and the figures are the medians
+over seeds (the paper reports medians over replications).  Prints one JSON
 line per (workload, N_B) and a summary table on stderr.
 
   python bench_sweep.py [--workloads NAME ...] [--min 64] [--max 131072]
-                        [--gens 100] [--evals 1000000] [--seed 0]
+                        [--gens 100] [--evals 1000000] [--seeds 1]
 """
 from __future__ import annotations
 
@@ -95,7 +97,7 @@ def main():
     ap.add_argument("--max", type=int, default=131072)
     ap.add_argument("--gens", type=int, default=100)
     ap.add_argument("--evals", type=int, default=1_000_000)
-    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--seeds", type=int, default=1)
     args = ap.parse_args()
 
     import torch
@@ -108,10 +110,14 @@ def main():
     for name in args.workloads:
         nb = args.min
         while nb <= args.max:
-            w = W.workload(name, batch=nb, seed=args.seed)
-            log(f"sweep: {name} N_B={nb}")
-            r = measure(w, args.gens, args.evals)
-            r.update(workload=name, evals_budget=args.evals, gens=args.gens, seed=args.seed)
+            runs = []
+            for seed in range(args.seeds):
+                log(f"sweep: {name} N_B={nb} seed {seed}")
+                runs.append(measure(W.workload(name, batch=nb, seed=seed), args.gens, args.evals))
+            r = {k: (sorted(x[k] for x in runs)[len(runs) // 2] if isinstance(runs[0][k], float)
+                     else runs[0][k]) for k in runs[0]}
+            r.update(workload=name, evals_budget=args.evals, gens=args.gens, seeds=args.seeds,
+                     per_seed_eval_per_s=[x["eval_per_s_paper"] for x in runs])
             print(json.dumps(r), flush=True)
             rows.append(r)
             nb *= 2
