@@ -14,7 +14,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liboracle.so")
 
-MAP_LOG, MAP_RSINPI, MAP_EXP, MAP_TANH, MAP_SIGMOID = 0, 1, 2, 3, 4
+MAP_RSINPI, MAP_EXP, MAP_TANH, MAP_SIGMOID = 1, 2, 3, 4
 
 
 class OrConfig(C.Structure):
@@ -47,9 +47,9 @@ def lib():
             "or_philox": (None, [u32p, u32p, u32p]),
             "or_u24": (C.c_float, [C.c_uint32]),
             "or_u24p": (C.c_float, [C.c_uint32]),
-            "or_box_muller": (None, [C.c_uint32, C.c_uint32, f32p]),
-            "or_logf": (C.c_float, [C.c_float]),
-            "or_turn_sincos": (None, [C.c_uint32, f32p]),
+            "or_normal": (C.c_float, [C.c_uint32]),
+            "or_normal_quantile": (C.c_double, [C.c_double]),
+            "or_normal_table": (None, [f32p]),
             "or_rsinpi": (C.c_float, [C.c_float]),
             "or_rsin_coef": (None, [C.POINTER(C.c_float)]),
             "or_expf": (C.c_float, [C.c_float]),
@@ -64,10 +64,7 @@ def lib():
             "or_key": (C.c_uint64, [C.c_float, C.c_int32, C.c_int32]),
             "or_map_f32": (None, [C.c_int32, f32p, f32p, C.c_int64]),
             "or_philox_many": (None, [u32p, u32p, u32p, C.c_int64]),
-            "or_box_muller_many": (None, [u32p, u32p, f32p, C.c_int64]),
-            "or_turn_sincos_many": (None, [u32p, f32p, C.c_int64]),
-            "or_turn_sincos_tab_many": (None, [u32p, f32p, C.c_int64]),
-            "or_log_k24_many": (None, [u32p, f32p, C.c_int64]),
+            "or_normal_many": (None, [u32p, f32p, C.c_int64]),
             "or_genotype_len": (C.c_int32, [C.POINTER(OrConfig)]),
             "or_env_len": (C.c_int32, [C.POINTER(OrConfig)]),
             "or_new": (P, [C.POINTER(OrConfig), C.c_int32]),
@@ -124,33 +121,25 @@ def philox(ctr, key) -> np.ndarray:
     return out
 
 
-def box_muller(xa, xb) -> np.ndarray:
-    xa = np.ascontiguousarray(np.asarray(xa, dtype=np.uint32).ravel())
-    xb = np.ascontiguousarray(np.asarray(xb, dtype=np.uint32).ravel())
-    out = np.zeros((xa.size, 2), dtype=np.float32)
-    lib().or_box_muller_many(_ptr(xa, C.c_uint32), _ptr(xb, C.c_uint32), _ptr(out, C.c_float),
-                             xa.size)
+def normal(x) -> np.ndarray:
+    """One standard normal per Philox word (the inverse-CDF sampler)."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.uint32).ravel())
+    out = np.zeros(x.size, dtype=np.float32)
+    lib().or_normal_many(_ptr(x, C.c_uint32), _ptr(out, C.c_float), x.size)
     return out
 
 
-def turn_sincos(m) -> np.ndarray:
-    m = np.ascontiguousarray(np.asarray(m, dtype=np.uint32).ravel())
-    out = np.zeros((m.size, 2), dtype=np.float32)
-    lib().or_turn_sincos_many(_ptr(m, C.c_uint32), _ptr(out, C.c_float), m.size)
-    return out
+def normal_quantile(p: float) -> float:
+    """Phi^-1(1 - p/2) in fp64, the sampler's table source."""
+    return float(lib().or_normal_quantile(float(p)))
 
 
-def turn_sincos_tab(m) -> np.ndarray:
-    m = np.ascontiguousarray(np.asarray(m, dtype=np.uint32).ravel())
-    out = np.zeros((m.size, 2), dtype=np.float32)
-    lib().or_turn_sincos_tab_many(_ptr(m, C.c_uint32), _ptr(out, C.c_float), m.size)
-    return out
+NORMAL_ROWS = 385
 
 
-def log_k24(k) -> np.ndarray:
-    k = np.ascontiguousarray(np.asarray(k, dtype=np.uint32).ravel())
-    out = np.zeros(k.size, dtype=np.float32)
-    lib().or_log_k24_many(_ptr(k, C.c_uint32), _ptr(out, C.c_float), k.size)
+def normal_table() -> np.ndarray:
+    out = np.zeros((NORMAL_ROWS, 4), dtype=np.float32)
+    lib().or_normal_table(_ptr(out, C.c_float))
     return out
 
 

@@ -82,150 +82,88 @@ float or_u24(uint32_t x) { return (float)(x >> 8) * 0x1p-24f; }
 float or_u24p(uint32_t x) { return (float)((x >> 8) + 1u) * 0x1p-24f; }
 
 /* ------------------------------------------------------------------------ */
-/* Own transcendental functions.  Built from +, -, *, fmaf, IEEE / and sqrt  */
-/* in a fixed order, with Taylor or atanh-series coefficients (exact         */
-/* rationals rounded once to fp32) and a Cody-Waite split of ln 2.           */
+/* Own transcendental functions.  Built from +, -, *, fmaf and IEEE / in a   */
+/* fixed order, with Taylor coefficients (exact rationals rounded once to    */
+/* fp32) and a Cody-Waite split of ln 2.                                     */
 /* ------------------------------------------------------------------------ */
 static const float kLn2Hi = 0x1.62e4p-1f;       /* ln 2 to 16 significant bits   */
 static const float kLn2Lo = 0x1.7f7d1cp-20f;    /* ln 2 - kLn2Hi, rounded        */
-static const float kPi = 0x1.921fb6p+1f;        /* pi rounded to fp32            */
-static const float kPiO2 = 0x1.921fb6p+0f;      /* pi/2 rounded to fp32          */
 static const float kLog2e = 0x1.715476p+0f;     /* 1/ln 2 rounded to fp32        */
 
-/* Natural log for positive normal x: x = 2^e m with m in [sqrt(2)/2, sqrt(2)),
- * ln m = 2 atanh(s), s = (m-1)/(m+1), series to s^9. */
-float or_logf(float x) {
-  uint32_t b = f2u(x);
-  int e = (int)((b >> 23) & 0xffu) - 127;
-  uint32_t mant = b & 0x7fffffu;
-  uint32_t mb = mant | 0x3f800000u;             /* m in [1, 2)                   */
-  if (mant > 0x3504f3u) {                       /* m > sqrt(2): halve it         */
-    mb -= 0x00800000u;
-    e += 1;
-  }
-  float m = u2f(mb);
-  float sr = (m - 1.0f) / (m + 1.0f);
-  float s2 = sr * sr;
-  float p = fmaf(s2, 2.0f / 9.0f, 2.0f / 7.0f);
-  p = fmaf(s2, p, 2.0f / 5.0f);
-  p = fmaf(s2, p, 2.0f / 3.0f);
-  float lm = fmaf(sr * s2, p, 2.0f * sr);
-  float fe = (float)e;
-  return fmaf(fe, kLn2Hi, fmaf(fe, kLn2Lo, lm));
-}
-
-/* sin and cos of x for |x| <= pi/4 by their Taylor series (to x^9, x^10). */
-static float sin_q(float x) {
-  float x2 = x * x;
-  float p = fmaf(x2, 1.0f / 362880.0f, -1.0f / 5040.0f);
-  p = fmaf(x2, p, 1.0f / 120.0f);
-  p = fmaf(x2, p, -1.0f / 6.0f);
-  return fmaf(x * x2, p, x);
-}
-static float cos_q(float x) {
-  float x2 = x * x;
-  float p = fmaf(x2, -1.0f / 3628800.0f, 1.0f / 40320.0f);
-  p = fmaf(x2, p, -1.0f / 720.0f);
-  p = fmaf(x2, p, 1.0f / 24.0f);
-  p = fmaf(x2, p, -0.5f);
-  return fmaf(x2, p, 1.0f);
-}
-
-/* cos and sin of the angle 2*pi*m/2^24 (m a 24-bit integer): nearest quarter
- * turn q (halves round up), remainder f = m/2^22 - q in [-1/2, 1/2), exact. */
-void or_turn_sincos(uint32_t m24, float out[2]) {
-  uint32_t m = m24 & 0xffffffu;
-  uint32_t qn = (m + 0x200000u) >> 22;          /* 0..4                          */
-  int32_t rem = (int32_t)m - (int32_t)(qn << 22);
-  float f = (float)rem * 0x1p-22f;
-  float x = f * kPiO2;
-  float sq = sin_q(x), cq = cos_q(x);
-  float c, sn;
-  switch (qn & 3u) {
-    case 0: c = cq; sn = sq; break;
-    case 1: c = -sq; sn = cq; break;
-    case 2: c = -cq; sn = -sq; break;
-    default: c = sq; sn = -cq; break;
-  }
-  out[0] = c;
-  out[1] = sn;
-}
-
 /* ------------------------------------------------------------------------ */
-/* Table-driven forms used by the Gaussian sampler.  The tables are built    */
-/* from the functions above (so they hold the same bits on every machine):   */
-/*   turn table  T[i] = (cos, sin) of 2 pi i / 256, i = 0..255               */
-/*   log table   bin i of m in [1, 2) = [1 + i/128, 1 + (i+1)/128): a        */
-/*               reciprocal R_i of the bin's midpoint c_i and L_i; bins from */
-/*               53 up (m >= 1.4140625, about sqrt 2) move a factor 2 into   */
-/*               the exponent and take L_i = -ln(2 R_i), the others          */
-/*               L_i = -ln R_i.  The first bin uses R = 1 and the last       */
-/*               R = 1/2 with L = 0, so that logs near 1 come out without    */
-/*               cancellation.                                               */
+/* Gaussian sampler.  Algorithm 2 draws eps1 ~ N(0, I) and eps2 ~ N(0, 1)    */
+/* without saying how.  Here each standard normal comes from one Philox word */
+/* x by inversion of the half-normal law: with k = (x >> 8) + 1 and          */
+/* p = k 2^-24 in (0, 1], the magnitude is z(p) = Phi^-1(1 - p/2), the       */
+/* point with P(|Z| >= z) = p, and bit 0 of x (which p does not use) is the  */
+/* sign.  z(p) is read from a table of cubic pieces: p = 2^(E-24) (1 + (j +  */
+/* t)/16) with E the binary exponent of k (0..24), j its next four bits and  */
+/* t in [0, 1) the remaining 19 bits / 2^19; row r = 16 E + j holds the      */
+/* monomial coefficients of the cubic in t that interpolates z at the four   */
+/* Chebyshev points of [0, 1], worked out in double and rounded once to fp32 */
+/* (coefficient i scaled by 2^(-19 i) so that the polynomial is evaluated    */
+/* in the integer t 2^19 directly).  Row 384 (k = 2^24, p = 1, z = 0) is     */
+/* zero.  Largest magnitude: z(2^-24) = 5.42.                                */
 /* ------------------------------------------------------------------------ */
-static float g_turn[256][2];
-static float g_logr[128], g_logl[128];
-static int g_tables_built = 0;
+static float g_ntab[OR_NORMAL_ROWS][4];
+static int g_ntab_built = 0;
 
-static void build_tables(void) {
-  if (g_tables_built) return;
-  for (uint32_t i = 0; i < 256; ++i) or_turn_sincos(i << 16, g_turn[i]);
-  for (int i = 0; i < 128; ++i) {
-    if (i == 0) { g_logr[i] = 1.0f; g_logl[i] = 0.0f; continue; }
-    if (i == 127) { g_logr[i] = 0.5f; g_logl[i] = 0.0f; continue; }
-    float c = 1.0f + ((float)i + 0.5f) / 128.0f;       /* exact */
-    float r = 1.0f / c;                                 /* IEEE division */
-    g_logr[i] = r;
-    g_logl[i] = -or_logf(i >= 53 ? r + r : r);
+/* z(p) = Phi^-1(1 - p/2) for p in (0, 1): the root of erfc(z / sqrt 2) = p,
+ * by 100 bisection steps on [0, 16] (erfc from the C library). */
+double or_normal_quantile(double p) {
+  const double inv_sqrt2 = 0.70710678118654752440;
+  double lo = 0.0, hi = 16.0;
+  for (int it = 0; it < 100; ++it) {
+    double mid = 0.5 * (lo + hi);
+    if (erfc(mid * inv_sqrt2) > p) lo = mid;
+    else hi = mid;
   }
-  g_tables_built = 1;
+  return 0.5 * (lo + hi);
 }
 
-/* cos and sin of 2 pi m / 2^24 (24-bit m) from the turn table: angle =
- * 2 pi (m >> 16) / 256 + delta, delta = (m & 0xffff) (2 pi 2^-24) in [0, 2 pi/256),
- * sin delta ~ delta - delta^3/6, cos delta ~ 1 - delta^2/2 + delta^4/24,
- * then the angle-addition formulas. */
-void or_turn_sincos_tab(uint32_t m24, float out[2]) {
-  build_tables();
-  uint32_t m = m24 & 0xffffffu;
-  const float* t = g_turn[m >> 16];
-  float d = (float)(m & 0xffffu) * (kPi * 0x1p-23f);
-  float d2 = d * d;
-  float sd = fmaf(d * d2, -1.0f / 6.0f, d);
-  float cd = fmaf(d2, fmaf(d2, 1.0f / 24.0f, -0.5f), 1.0f);
-  out[0] = fmaf(t[0], cd, -(t[1] * sd));
-  out[1] = fmaf(t[1], cd, t[0] * sd);
+static void build_normal_table(void) {
+  if (g_ntab_built) return;
+  /* Chebyshev points of [0, 1]: (1 -+ cos(pi/8)) / 2, (1 -+ cos(3 pi/8)) / 2 */
+  const double r2 = sqrt(2.0);
+  const double ca = 0.5 * sqrt(2.0 + r2), cb = 0.5 * sqrt(2.0 - r2);
+  const double t[4] = {0.5 * (1.0 - ca), 0.5 * (1.0 - cb), 0.5 * (1.0 + cb), 0.5 * (1.0 + ca)};
+  for (int r = 0; r < OR_NORMAL_ROWS - 1; ++r) {
+    int E = r >> 4, j = r & 15;
+    double f[4];
+    for (int i = 0; i < 4; ++i)
+      f[i] = or_normal_quantile(ldexp(1.0 + ((double)j + t[i]) / 16.0, E - 24));
+    /* Newton divided differences: f[i] becomes z[t_0, ..., t_i] */
+    for (int k = 1; k < 4; ++k)
+      for (int i = 3; i >= k; --i) f[i] = (f[i] - f[i - 1]) / (t[i] - t[i - k]);
+    /* Newton form f0 + (t - t0)(f1 + (t - t1)(f2 + (t - t2) f3)) -> powers of
+     * t, innermost factor first: m <- m (t - t_k) + f_k for k = 2, 1, 0 */
+    double m[4] = {f[3], 0.0, 0.0, 0.0};
+    for (int k = 2; k >= 0; --k) {
+      for (int i = 3; i >= 1; --i) m[i] = m[i - 1] - t[k] * m[i];
+      m[0] = f[k] - t[k] * m[0];
+    }
+    for (int i = 0; i < 4; ++i) g_ntab[r][i] = (float)ldexp(m[i], -19 * i);
+  }
+  for (int i = 0; i < 4; ++i) g_ntab[OR_NORMAL_ROWS - 1][i] = 0.0f;
+  g_ntab_built = 1;
 }
 
-/* ln(k 2^-24) for an integer k in [1, 2^24] from the log table: k = 2^E m,
- * m in [1, 2), bin i = top 7 fraction bits of m, t = m R_i - 1 (one rounding),
- * ln(m 2^-f) = L_i + t - t^2/2 + t^3/3 - t^4/4 with f = 1 for bins i >= 53
- * (else 0), and exponent E - 24 + f. */
-float or_log_k24(uint32_t k) {
-  build_tables();
-  float kf = (float)k;
-  uint32_t b = f2u(kf);
-  int e = (int)(b >> 23) - 127 - 24;
-  uint32_t i = (b >> 16) & 0x7fu;
-  if (i >= 53u) e += 1;
-  float m = u2f((b & 0x7fffffu) | 0x3f800000u);
-  float t = fmaf(m, g_logr[i], -1.0f);
-  float q = fmaf(t, -0.25f, 1.0f / 3.0f);
-  q = fmaf(t, q, -0.5f);
-  float lnm = g_logl[i] + fmaf(t * t, q, t);
-  float fe = (float)e;
-  return fmaf(fe, kLn2Hi, fmaf(fe, kLn2Lo, lnm));
+void or_normal_table(float* out) {
+  build_normal_table();
+  memcpy(out, g_ntab, sizeof(g_ntab));
 }
 
-/* Box-Muller (1958): two standard normals from two Philox words.  The radius
- * uses the (0,1] uniform ((xa >> 8) + 1) 2^-24 so ln never sees 0; the angle
- * uses the top 24 bits of xb. */
-void or_box_muller(uint32_t xa, uint32_t xb, float out[2]) {
-  float r = sqrtf(-2.0f * or_log_k24((xa >> 8) + 1u));
-  float cs[2];
-  or_turn_sincos_tab(xb >> 8, cs);
-  out[0] = r * cs[0];
-  out[1] = r * cs[1];
+/* One standard normal from one Philox word (see above): Horner's rule from
+ * the cubic term, then the sign of bit 0. */
+float or_normal(uint32_t x) {
+  build_normal_table();
+  uint32_t k = (x >> 8) + 1u;
+  uint32_t b = f2u((float)k);                    /* k <= 2^24: exact           */
+  uint32_t r = (b >> 19) - (127u << 4);          /* 16 E + j                   */
+  float tf = (float)(b & 0x7ffffu);              /* t 2^19, exact              */
+  const float* c = g_ntab[r];
+  float z = fmaf(tf, fmaf(tf, fmaf(tf, c[3], c[2]), c[1]), c[0]);
+  return (x & 1u) ? -z : z;
 }
 
 /* sqrt(20) sin(pi x), up to sign, for the Rastrigin term.  r = x - rint(x)
@@ -632,11 +570,8 @@ void or_setup(or_state* s) {
   int32_t ne = or_env_len(c);
   for (int32_t e = 0; e < ne; ++e) {
     uint32_t x[4];
-    float z[4];
     draw(s, (uint32_t)(e / 4), 0, 0, TAG_ENV, x);
-    or_box_muller(x[0], x[1], z);
-    or_box_muller(x[2], x[3], z + 2);
-    s->env[e] = 0.1f * z[e % 4];
+    s->env[e] = 0.1f * or_normal(x[e % 4]);
   }
 }
 
@@ -706,20 +641,14 @@ static void make_offspring(or_state* s, uint32_t g, int32_t j, int32_t nocc, flo
   draw(s, 0, (uint32_t)j, g, TAG_SELECT, x);
   int32_t p1 = s->occ_list[(uint32_t)(((uint64_t)x[0] * (uint64_t)(uint32_t)nocc) >> 32)];
   int32_t p2 = s->occ_list[(uint32_t)(((uint64_t)x[1] * (uint64_t)(uint32_t)nocc) >> 32)];
-  float z[2];
-  or_box_muller(x[2], x[3], z);
-  float lambda = c->line_sigma * z[0];
+  float lambda = c->line_sigma * or_normal(x[2]);
   const float* t1 = s->geno + (size_t)p1 * n;
   const float* t2 = s->geno + (size_t)p2 * n;
-  float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  uint32_t y[4] = {0, 0, 0, 0};
   for (int32_t i = 0; i < n; ++i) {
-    if ((i & 3) == 0) { /* block i/4 holds the normals of genes i .. i+3 */
-      uint32_t y[4];
-      draw(s, (uint32_t)(i >> 2), (uint32_t)j, g, TAG_ISO, y);
-      or_box_muller(y[0], y[1], e);
-      or_box_muller(y[2], y[3], e + 2);
-    }
-    float eps1 = e[i & 3];
+    /* block i/4 holds the words of genes i .. i+3, one normal each */
+    if ((i & 3) == 0) draw(s, (uint32_t)(i >> 2), (uint32_t)j, g, TAG_ISO, y);
+    float eps1 = or_normal(y[i & 3]);
     out[i] = fmaf(lambda, t2[i] - t1[i], fmaf(c->iso_sigma, eps1, t1[i]));
   }
   par[0] = p1;
@@ -855,11 +784,11 @@ void or_map_f32(int32_t fn, const float* in, float* out, int64_t count) {
   for (int64_t i = 0; i < count; ++i) {
     float x = in[i];
     switch (fn) {
-      case 0: out[i] = or_logf(x); break;
       case 1: out[i] = or_rsinpi(x); break;
       case 2: out[i] = or_expf(x); break;
       case 3: out[i] = or_tanhf(x); break;
-      default: out[i] = or_sigmoidf(x); break;
+      case 4: out[i] = or_sigmoidf(x); break;
+      default: out[i] = NAN; break;
     }
   }
 }
@@ -868,18 +797,6 @@ void or_philox_many(const uint32_t* ctr, const uint32_t key[2], uint32_t* out, i
   for (int64_t i = 0; i < count; ++i) or_philox(ctr + 4 * i, key, out + 4 * i);
 }
 
-void or_box_muller_many(const uint32_t* xa, const uint32_t* xb, float* out, int64_t count) {
-  for (int64_t i = 0; i < count; ++i) or_box_muller(xa[i], xb[i], out + 2 * i);
-}
-
-void or_turn_sincos_many(const uint32_t* m, float* out, int64_t count) {
-  for (int64_t i = 0; i < count; ++i) or_turn_sincos(m[i], out + 2 * i);
-}
-
-void or_turn_sincos_tab_many(const uint32_t* m, float* out, int64_t count) {
-  for (int64_t i = 0; i < count; ++i) or_turn_sincos_tab(m[i], out + 2 * i);
-}
-
-void or_log_k24_many(const uint32_t* k, float* out, int64_t count) {
-  for (int64_t i = 0; i < count; ++i) out[i] = or_log_k24(k[i]);
+void or_normal_many(const uint32_t* x, float* out, int64_t count) {
+  for (int64_t i = 0; i < count; ++i) out[i] = or_normal(x[i]);
 }

@@ -20,6 +20,10 @@ extern "C" {
 enum { OR_RASTRIGIN = 0, OR_SPHERE = 1, OR_RASTRIGIN_PROJ = 2, OR_MLP = 3 };
 enum { OR_GRID = 0, OR_CVT = 1 };
 
+/* Rows of the Gaussian sampler's table (sixteen per binade of k = 1..2^24,
+ * and one for k = 2^24). */
+#define OR_NORMAL_ROWS 385
+
 typedef struct {
   int32_t task, tess;
   int32_t n;            /* genotype length; ignored for OR_MLP (derived)       */
@@ -44,9 +48,9 @@ typedef struct or_state or_state;
 void     or_philox(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
 float    or_u24(uint32_t x);
 float    or_u24p(uint32_t x);
-void     or_box_muller(uint32_t xa, uint32_t xb, float out[2]);
-float    or_logf(float x);
-void     or_turn_sincos(uint32_t m24, float out[2]);   /* cos, sin of 2*pi*m/2^24 */
+float    or_normal(uint32_t x);               /* one standard normal per word */
+double   or_normal_quantile(double p);        /* Phi^-1(1 - p/2), fp64        */
+void     or_normal_table(float* out);         /* [OR_NORMAL_ROWS][4]          */
 float    or_rsinpi(float x);          /* sqrt(20) sin(pi x), up to sign */
 void     or_rsin_coef(float out[6]);  /* its six polynomial coefficients */
 float    or_expf(float x);
@@ -66,13 +70,7 @@ uint64_t or_key(float f, int32_t j, int32_t batch);
 void     or_map_f32(int32_t fn, const float* in, float* out, int64_t count);
 void     or_philox_many(const uint32_t* ctr, const uint32_t key[2], uint32_t* out,
                         int64_t count);
-void     or_box_muller_many(const uint32_t* xa, const uint32_t* xb, float* out,
-                            int64_t count);
-void     or_turn_sincos_many(const uint32_t* m, float* out, int64_t count);
-void     or_turn_sincos_tab(uint32_t m24, float out[2]);
-float    or_log_k24(uint32_t k);
-void     or_turn_sincos_tab_many(const uint32_t* m, float* out, int64_t count);
-void     or_log_k24_many(const uint32_t* k, float* out, int64_t count);
+void     or_normal_many(const uint32_t* x, float* out, int64_t count);
 
 /* ---- the run ---- */
 int32_t   or_genotype_len(const or_config* cfg);

@@ -15,38 +15,6 @@ def ulp_err(got, ref):
     return np.abs(got - ref) / spacing
 
 
-def test_log_exhaustive_on_box_muller_domain():
-    # every value the Box-Muller radius can feed to log: k * 2^-24, k = 1..2^24
-    k = np.arange(1, (1 << 24) + 1, dtype=np.float64)
-    x = (k / 2.0**24).astype(np.float32)
-    got = O.map_f32(O.MAP_LOG, x)
-    ref = np.log(x.astype(np.float64))
-    ok = ref != 0
-    assert got[~ok].tolist() == [0.0]           # log 1 = 0 exactly
-    assert ulp_err(got[ok], ref[ok]).max() <= 3.0
-
-
-def test_table_log_exhaustive_on_box_muller_domain():
-    # the table-driven ln(k 2^-24) the sampler uses, for every k = 1..2^24
-    k = np.arange(1, (1 << 24) + 1, dtype=np.uint32)
-    got = O.log_k24(k)
-    ref = np.log(k.astype(np.float64) / 2.0**24)
-    ok = ref != 0
-    assert got[~ok].tolist() == [0.0]
-    assert ulp_err(got[ok], ref[ok]).max() <= 2.5
-    # monotone in k: a property any reordering of bins or sign slip breaks
-    assert np.all(np.diff(got.astype(np.float64)) >= 0)
-
-
-def test_log_wide_range():
-    x = np.float32(2.0) ** np.linspace(-125, 127, 200001).astype(np.float32)
-    got = O.map_f32(O.MAP_LOG, x)
-    ref = np.log(x.astype(np.float64))
-    assert ulp_err(got, ref).max() <= 3.0
-    for e in range(-20, 21):
-        assert abs(O.map_f32(O.MAP_LOG, [2.0**e])[0] - e * np.log(2.0)) <= 4e-7 * max(1, abs(e))
-
-
 def test_scaled_sinpi():
     # sqrt(20) sin(pi x) up to sign, the Rastrigin term's sine
     x = np.linspace(-12, 12, 480001).astype(np.float32)

@@ -3,9 +3,11 @@
 * Philox4x32-10 against rocRAND's open-source engine compiled on the host
   (a library routine), over random counters and keys.
 * The 24-bit uniforms at their exact end points.
-* The quarter-turn sine/cosine against numpy's fp64 sin/cos.
-* Box-Muller against the fp64 formula sqrt(-2 ln u1) (cos, sin)(2 pi u2) and
-  against N(0,1) by moments and a Kolmogorov-Smirnov test.
+* The inverse-CDF Gaussian sampler: its fp64 quantile against scipy's ndtri
+  (Cephes) and textbook points, every one of its 2^24 magnitudes against
+  ndtri, its table against the quantile at the interpolation points, and its
+  output on Philox words against N(0,1) by moments and a Kolmogorov-Smirnov
+  test.
 """
 import os
 import shutil
@@ -14,6 +16,7 @@ import subprocess
 import numpy as np
 import pytest
 from scipy import stats
+from scipy.special import erfc, ndtri
 
 from oracle import oracle as O
 
@@ -68,61 +71,72 @@ def test_u24_end_points():
     assert O.u24(0x80000000) == 0.5
 
 
-def test_turn_sincos_against_fp64():
-    m = np.concatenate([
-        np.arange(0, 1 << 24, 97, dtype=np.uint32),
-        # around every quarter turn and the half-way points between them
-        np.array([(q << 22) + d for q in range(4) for d in (-1, 0, 1)] +
-                 [(q << 22) + (1 << 21) + d for q in range(4) for d in (-1, 0, 1)],
-                 dtype=np.int64).astype(np.uint32) & 0xFFFFFF,
-    ])
-    cs = O.turn_sincos(m).astype(np.float64)
-    ang = 2.0 * np.pi * m.astype(np.float64) / 2.0**24
-    assert np.max(np.abs(cs[:, 0] - np.cos(ang))) < 2.5e-7
-    assert np.max(np.abs(cs[:, 1] - np.sin(ang))) < 2.5e-7
-    exact = O.turn_sincos(np.array([0, 1 << 22, 2 << 22, 3 << 22], dtype=np.uint32))
-    np.testing.assert_array_equal(exact, [[1, 0], [0, 1], [-1, 0], [0, -1]])
+def _k_of(x):
+    return (np.asarray(x, dtype=np.uint32) >> 8).astype(np.float64) + 1.0
 
 
-def test_table_turn_sincos_against_fp64():
-    # the table-driven (cos, sin) of 2 pi m / 2^24 that the sampler uses
-    m = np.concatenate([np.arange(0, 1 << 24, 37, dtype=np.uint32),
-                        (np.arange(256, dtype=np.uint32) << 16),           # table points
-                        (np.arange(256, dtype=np.uint32) << 16) + 0xFFFF])  # bin ends
-    cs = O.turn_sincos_tab(m).astype(np.float64)
-    ang = 2.0 * np.pi * m.astype(np.float64) / 2.0**24
-    assert np.max(np.abs(cs[:, 0] - np.cos(ang))) < 2.0e-7
-    assert np.max(np.abs(cs[:, 1] - np.sin(ang))) < 2.0e-7
-    # at a table point the remainder is 0 and the entry comes back unchanged
-    pts = (np.arange(256, dtype=np.uint32) << 16)
-    np.testing.assert_array_equal(O.turn_sincos_tab(pts), O.turn_sincos(pts))
+def test_normal_quantile_against_scipy_and_closed_forms():
+    # the fp64 source of the table: Phi^-1(1 - p/2) = -ndtri(p/2) (Cephes)
+    for p in np.concatenate([np.logspace(-9, -1e-9, 300), [0.05, 0.01, 0.5, 0.999]]):
+        ref = -ndtri(p / 2.0)
+        assert abs(O.normal_quantile(p) - ref) <= 1e-13 * max(1.0, ref), p
+    # textbook two-sided points and P(|Z| >= 1) = erfc(1/sqrt 2)
+    assert abs(O.normal_quantile(0.05) - 1.959963984540054) < 1e-14
+    assert abs(O.normal_quantile(0.01) - 2.5758293035489004) < 1e-14
+    assert abs(O.normal_quantile(erfc(1.0 / np.sqrt(2.0))) - 1.0) < 1e-14
 
 
-def test_box_muller_against_fp64_formula():
-    rng = np.random.default_rng(7)
-    xa = rng.integers(0, 2**32, size=200000, dtype=np.uint64).astype(np.uint32)
-    xb = rng.integers(0, 2**32, size=200000, dtype=np.uint64).astype(np.uint32)
-    z = O.box_muller(xa, xb).astype(np.float64)
-    u1 = ((xa >> 8).astype(np.float64) + 1.0) / 2.0**24
-    u2 = (xb >> 8).astype(np.float64) / 2.0**24
-    r = np.sqrt(-2.0 * np.log(u1))
-    ref = np.stack([r * np.cos(2 * np.pi * u2), r * np.sin(2 * np.pi * u2)], axis=1)
-    err = np.abs(z - ref) / np.maximum(1.0, np.abs(ref))
-    assert err.max() < 1e-6, err.max()
+def test_normal_exhaustive_against_scipy():
+    # every magnitude the sampler can return: k = 1..2^24, p = k 2^-24,
+    # |z| = Phi^-1(1 - p/2) = -ndtri(k 2^-25); the low byte of the word other
+    # than bit 0 is ignored, bit 0 is the sign
+    k = np.arange(1, (1 << 24) + 1, dtype=np.uint64)
+    low = np.random.default_rng(3).integers(0, 128, size=k.size, dtype=np.uint64) << 1
+    x = (((k - 1) << 8) | low).astype(np.uint32)
+    z = O.normal(x).astype(np.float64)
+    ref = -ndtri(k.astype(np.float64) * 2.0**-25)
+    err = np.abs(z - ref)
+    assert err.max() <= 5e-7, err.max()
+    spacing = np.spacing(np.maximum(np.abs(z), 2.0**-7).astype(np.float32)).astype(np.float64)
+    assert (err / spacing).max() <= 4.0
+    assert z[-1] == 0.0 and z[0] > 5.41                 # p = 1 and p = 2^-24
+    assert np.all(np.diff(z) <= 0.0)                    # |z| falls as p grows
+    neg = O.normal(x | 1).astype(np.float64)
+    np.testing.assert_array_equal(neg[:-1], -z[:-1])
 
 
-def test_box_muller_is_standard_normal():
+def test_normal_table_interpolates_at_chebyshev_points():
+    # row 16 E + j covers p = 2^(E-24) (1 + (j + t)/16), t in [0, 1); its
+    # stored cubic in t 2^19 meets the fp64 quantile at the four Chebyshev
+    # points of [0, 1] up to the fp32 rounding of the coefficients
+    tab = O.normal_table().astype(np.float64)
+    assert tab.shape == (385, 4) and np.all(tab[384] == 0.0)
+    nodes = (1.0 - np.cos((2 * np.arange(4) + 1) * np.pi / 8)) / 2.0
+    for r in range(0, 384, 7):
+        e, j = r >> 4, r & 15
+        for t in nodes:
+            q = O.normal_quantile(2.0 ** (e - 24) * (1.0 + (j + t) / 16.0))
+            u = t * 2.0**19
+            got = tab[r, 0] + u * (tab[r, 1] + u * (tab[r, 2] + u * tab[r, 3]))
+            assert abs(got - q) <= 4e-7 * max(1.0, q), (r, t, got, q)
+
+
+def test_normal_is_standard_normal():
     j = np.arange(1 << 19, dtype=np.uint32)
     ctr = np.stack([j, np.zeros_like(j), np.ones_like(j), np.full_like(j, 2)], axis=1)
     x = O.philox(ctr, [12345, 678])
-    z = np.concatenate([O.box_muller(x[:, 0], x[:, 1]), O.box_muller(x[:, 2], x[:, 3])])
-    z = z.astype(np.float64)
-    for col in range(2):
+    z = O.normal(x.ravel()).astype(np.float64).reshape(-1, 4)
+    for col in range(4):
         v = z[:, col]
         assert abs(v.mean()) < 5e-3
         assert abs(v.var() - 1.0) < 1e-2
         assert abs(stats.skew(v)) < 1e-2
         assert abs(stats.kurtosis(v)) < 2e-2
         assert stats.kstest(v, "norm").pvalue > 1e-3
-    # the two members of a pair are uncorrelated
-    assert abs(np.corrcoef(z[:, 0], z[:, 1])[0, 1]) < 5e-3
+    # normals from the words of one block are uncorrelated
+    c = np.corrcoef(z.T)
+    assert np.max(np.abs(c - np.eye(4))) < 5e-3
+    # signs balanced, and the magnitude independent of the sign bit
+    sgn = z < 0
+    assert abs(sgn.mean() - 0.5) < 2e-3
+    assert abs(np.abs(z[sgn]).mean() - np.abs(z[~sgn]).mean()) < 5e-3
