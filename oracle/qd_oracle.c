@@ -93,12 +93,12 @@ static const float kLog2e = 0x1.715476p+0f;     /* 1/ln 2 rounded to fp32       
 /* ------------------------------------------------------------------------ */
 /* Gaussian sampler.  Algorithm 2 draws eps1 ~ N(0, I) and eps2 ~ N(0, 1)    */
 /* without saying how.  Here each standard normal comes from one Philox word */
-/* x by inversion of the half-normal law: with k = (x >> 8) + 1 and          */
+/* x by inversion of the half-normal law: with k = (x & 0xffffff) + 1 and    */
 /* p = k 2^-24 in (0, 1], the magnitude is z(p) = Phi^-1(1 - p/2), the       */
-/* point with P(|Z| >= z) = p, and bit 0 of x (which p does not use) is the  */
-/* sign.  z(p) is read from a table of cubic pieces: p = 2^(E-24) (1 + (j +  */
-/* t)/16) with E the binary exponent of k (0..24), j its next four bits and  */
-/* t in [0, 1) the remaining 19 bits / 2^19; row r = 16 E + j holds the      */
+/* point with P(|Z| >= z) = p, and bit 31 of x is the sign (bits 24..30 are  */
+/* not used).  z(p) is read from a table of cubic pieces: p = 2^(E-24) (1 +  */
+/* (j + t)/16) with E the binary exponent of k (0..24), j its next four bits */
+/* and t in [0, 1) the remaining 19 bits / 2^19; row r = 16 E + j holds the  */
 /* monomial coefficients of the cubic in t that interpolates z at the four   */
 /* Chebyshev points of [0, 1], worked out in double and rounded once to fp32 */
 /* (coefficient i scaled by 2^(-19 i) so that the polynomial is evaluated    */
@@ -154,16 +154,16 @@ void or_normal_table(float* out) {
 }
 
 /* One standard normal from one Philox word (see above): Horner's rule from
- * the cubic term, then the sign of bit 0. */
+ * the cubic term, then the sign of bit 31. */
 float or_normal(uint32_t x) {
   build_normal_table();
-  uint32_t k = (x >> 8) + 1u;
+  uint32_t k = (x & 0xffffffu) + 1u;
   uint32_t b = f2u((float)k);                    /* k <= 2^24: exact           */
   uint32_t r = (b >> 19) - (127u << 4);          /* 16 E + j                   */
   float tf = (float)(b & 0x7ffffu);              /* t 2^19, exact              */
   const float* c = g_ntab[r];
   float z = fmaf(tf, fmaf(tf, fmaf(tf, c[3], c[2]), c[1]), c[0]);
-  return (x & 1u) ? -z : z;
+  return (x >> 31) ? -z : z;
 }
 
 /* sqrt(20) sin(pi x), up to sign, for the Rastrigin term.  r = x - rint(x)

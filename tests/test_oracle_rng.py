@@ -71,10 +71,6 @@ def test_u24_end_points():
     assert O.u24(0x80000000) == 0.5
 
 
-def _k_of(x):
-    return (np.asarray(x, dtype=np.uint32) >> 8).astype(np.float64) + 1.0
-
-
 def test_normal_quantile_against_scipy_and_closed_forms():
     # the fp64 source of the table: Phi^-1(1 - p/2) = -ndtri(p/2) (Cephes)
     for p in np.concatenate([np.logspace(-9, -1e-9, 300), [0.05, 0.01, 0.5, 0.999]]):
@@ -88,11 +84,11 @@ def test_normal_quantile_against_scipy_and_closed_forms():
 
 def test_normal_exhaustive_against_scipy():
     # every magnitude the sampler can return: k = 1..2^24, p = k 2^-24,
-    # |z| = Phi^-1(1 - p/2) = -ndtri(k 2^-25); the low byte of the word other
-    # than bit 0 is ignored, bit 0 is the sign
+    # |z| = Phi^-1(1 - p/2) = -ndtri(k 2^-25); k - 1 is the low 24 bits of
+    # the word, bits 24..30 are ignored, bit 31 is the sign
     k = np.arange(1, (1 << 24) + 1, dtype=np.uint64)
-    low = np.random.default_rng(3).integers(0, 128, size=k.size, dtype=np.uint64) << 1
-    x = (((k - 1) << 8) | low).astype(np.uint32)
+    mid = np.random.default_rng(3).integers(0, 128, size=k.size, dtype=np.uint64) << 24
+    x = ((k - 1) | mid).astype(np.uint32)
     z = O.normal(x).astype(np.float64)
     ref = -ndtri(k.astype(np.float64) * 2.0**-25)
     err = np.abs(z - ref)
@@ -101,7 +97,7 @@ def test_normal_exhaustive_against_scipy():
     assert (err / spacing).max() <= 4.0
     assert z[-1] == 0.0 and z[0] > 5.41                 # p = 1 and p = 2^-24
     assert np.all(np.diff(z) <= 0.0)                    # |z| falls as p grows
-    neg = O.normal(x | 1).astype(np.float64)
+    neg = O.normal(x | np.uint32(0x80000000)).astype(np.float64)
     np.testing.assert_array_equal(neg[:-1], -z[:-1])
 
 
