@@ -33,10 +33,19 @@
 extern "C" {
 #endif
 
-#define QD_ABI_VERSION 4u
+#define QD_ABI_VERSION 5u
 
 /* Candidate slots per fine bucket of a two-dimensional CVT (see QD_BUF_CAND_*). */
 #define QD_CAND_SLOTS 16
+
+/* Rows of the Gaussian sampler's table.  Algorithm 2 draws eps1 ~ N(0, I) and
+ * eps2 ~ N(0, 1); each normal comes from one random word x by inversion:
+ * k = (x & 0xffffff) + 1, p = k 2^-24, magnitude Phi^-1(1 - p/2), sign = bit
+ * 31 of x.
+ * Row 16 E + j (E = binary exponent of k, j = its next four bits) holds the
+ * coefficients (c0, c1, c2, c3) of a cubic in the remaining 19 bits of k;
+ * row 384 (k = 2^24) is zero. */
+#define QD_NORMAL_ROWS 385
 
 typedef enum {
   QD_OK = 0,
@@ -117,6 +126,8 @@ enum {
   QD_BUF_OFF_BANK,         /* u8  [N_B] genotype banks of parent 1 (bit 0), 2 (bit 1) */
   QD_BUF_OFF_GENO,         /* f32 [N_B][row_stride] (keep_offspring only)            */
   QD_BUF_STATS,            /* f64 [8]   device-side statistics                        */
+  QD_BUF_NORMAL_TAB,       /* f32x4 [QD_NORMAL_ROWS] Gaussian sampler table, written  */
+                           /*   by qd_archive_init (see QD_NORMAL_ROWS)               */
   QD_NUM_BUFFERS
 };
 
@@ -159,8 +170,11 @@ qd_status qd_layout_query(const qd_config* cfg, qd_layout* out);
  * draws, then cvt_iters Lloyd iterations over cvt_samples uniform points: each
  * point to its nearest centroid, each centroid that received points to their
  * mean) and the synthetic environment from their Philox streams, an empty
- * archive, N_B random genotypes evaluated and inserted.  Asynchronous: returns once the
- * work is enqueued.  *out receives a host handle owned by the library (free it
+ * archive, N_B random genotypes evaluated and inserted.  The Gaussian sampler's
+ * table (QD_BUF_NORMAL_TAB) is built on the host (once per process) and
+ * copied into the workspace on `stream` ahead of that work; the host copy
+ * lives until the process ends.  Asynchronous: returns once the work is
+ * enqueued.  *out receives a host handle owned by the library (free it
  * with qd_archive_destroy).  The workspace must stay valid until then. */
 qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t workspace_bytes,
                           void* stream, qd_archive** out);
@@ -204,13 +218,12 @@ qd_status qd_set_kernel_timing(qd_archive* h, uint32_t kernel_mask);
  * them.  ms and counts must hold QD_NUM_KERNELS entries. */
 qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts);
 
-/* Self-check of the short division and square-root sequences the kernels use
- * in place of IEEE division and square root, over every input each can
- * receive: mismatches[0] counts the Box-Muller radius inputs (all 2^24) whose
- * result differs from the IEEE-arithmetic definition, mismatches[1] the fp32
- * inputs of tanh (all 2^32), mismatches[2] those of sigmoid in [-1, 1]
- * (zeros mean bit-identical results).  d_scratch: 24 bytes of device memory
- * owned by the caller, 8-byte aligned.  Synchronises `stream`. */
+/* Self-check of the short division sequences the kernels use in place of
+ * IEEE division, over every input each can receive: mismatches[0] counts the
+ * fp32 inputs of tanh (all 2^32) whose result differs from the IEEE-arithmetic
+ * definition, mismatches[1] those of sigmoid in [-1, 1] (zeros mean
+ * bit-identical results).  d_scratch: 16 bytes of device memory owned by the
+ * caller, 8-byte aligned.  Synchronises `stream`. */
 qd_status qd_check_fast_arith(void* d_scratch, void* stream, uint64_t* mismatches);
 
 /* Frees the host handle (not the workspace).  NULL is accepted. */

@@ -12,6 +12,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/qd.h"
+
 namespace qd {
 
 // ---------------------------------------------------------------------------
@@ -52,12 +54,9 @@ __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
 __device__ __forceinline__ float unit24(uint32_t x) {        // [0, 1)
   return (float)(x >> 8) * 0x1p-24f;
 }
-__device__ __forceinline__ float unit24_open0(uint32_t x) {  // (0, 1]
-  return (float)((x >> 8) + 1u) * 0x1p-24f;
-}
 
 // ---------------------------------------------------------------------------
-// fp32 functions from +, -, *, fma, IEEE division and square root.
+// fp32 functions from +, -, *, fma and IEEE division.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float fma32(float a, float b, float c) {
   return __builtin_fmaf(a, b, c);
@@ -65,156 +64,46 @@ __device__ __forceinline__ float fma32(float a, float b, float c) {
 
 constexpr float kLn2Hi = 0x1.62e4p-1f;      // ln 2, 16 leading bits
 constexpr float kLn2Lo = 0x1.7f7d1cp-20f;   // remainder of ln 2
-constexpr float kPi = 0x1.921fb6p+1f;
-constexpr float kHalfPi = 0x1.921fb6p+0f;
 constexpr float kLog2e = 0x1.715476p+0f;
 
-// Square root of a positive normal x (or +-0) without the small-input
-// scaling: hardware estimate, then the neighbour one unit in the last place
-// below or above is taken when the fma residual says the estimate rounded
-// the wrong way.  (For x = +-0 both neighbours fail their test, so +-0 comes
-// back unchanged.)  On every input the Box-Muller radius can feed it this
-// returns the IEEE square root bit for bit; the library checks that over all
-// of them (qd_check_fast_arith).
-__device__ __forceinline__ float sqrt_normal(float x) {
-  const float s = __builtin_amdgcn_sqrtf(x);
-  const float dn = __uint_as_float(__float_as_uint(s) - 1u);
-  const float up = __uint_as_float(__float_as_uint(s) + 1u);
-  const float r = fma32(-dn, s, x) <= 0.0f ? dn : s;
-  return fma32(-up, s, x) > 0.0f ? up : r;
-}
-
-// ln x for positive normal x.  x = 2^e m, m folded into [sqrt(1/2), sqrt(2));
-// ln m = 2 atanh(s) with s = (m - 1)/(m + 1), odd series through s^9.  Used
-// to fill the log table of the Gaussian sampler.
-__device__ __forceinline__ float log_pos(float x) {
-  const uint32_t bits = __float_as_uint(x);
-  const uint32_t frac = bits & 0x7fffffu;
-  const bool fold = frac > 0x3504f3u;
-  const int e = (int)(bits >> 23) - 127 + (fold ? 1 : 0);
-  const float m = __uint_as_float((frac | 0x3f800000u) - (fold ? 0x00800000u : 0u));
-  const float s = (m - 1.0f) / (m + 1.0f);
-  const float s2 = s * s;
-  float p = fma32(s2, 2.0f / 9.0f, 2.0f / 7.0f);
-  p = fma32(s2, p, 2.0f / 5.0f);
-  p = fma32(s2, p, 2.0f / 3.0f);
-  const float lnm = fma32(s * s2, p, s + s);
-  const float fe = (float)e;
-  return fma32(fe, kLn2Hi, fma32(fe, kLn2Lo, lnm));
-}
-
-// sin / cos of x, |x| <= pi/4: Taylor polynomials through x^9 and x^10.
-__device__ __forceinline__ float sin_small(float x) {
-  const float x2 = x * x;
-  float p = fma32(x2, 1.0f / 362880.0f, -1.0f / 5040.0f);
-  p = fma32(x2, p, 1.0f / 120.0f);
-  p = fma32(x2, p, -1.0f / 6.0f);
-  return fma32(x * x2, p, x);
-}
-__device__ __forceinline__ float cos_small(float x) {
-  const float x2 = x * x;
-  float p = fma32(x2, -1.0f / 3628800.0f, 1.0f / 40320.0f);
-  p = fma32(x2, p, -1.0f / 720.0f);
-  p = fma32(x2, p, 1.0f / 24.0f);
-  p = fma32(x2, p, -0.5f);
-  return fma32(x2, p, 1.0f);
-}
-
-// (cos, sin) of 2 pi m / 2^24 for a 24-bit m: the nearest quarter turn q
-// (halves rounding up) is split off in integers, leaving (pi/2) f with
-// f = m / 2^22 - q, |f| <= 1/2, exactly.
-__device__ __forceinline__ float2 turn_cos_sin(uint32_t m) {
-  const uint32_t t = m + 0x200000u;
-  const uint32_t q = t >> 22;
-  // f * pi/2 with f = rem 2^-22: the power-of-two factor is exact, so it is
-  // folded into the constant and the product still rounds once
-  const float x = (float)((int32_t)(t & 0x3fffffu) - 0x200000) * (kHalfPi * 0x1p-22f);
-  const float s = sin_small(x), c = cos_small(x);
-  // quarter turns q = 0..3 (4 = 0): (c, s), (-s, c), (-c, -s), (s, -c),
-  // written as a swap on odd q and sign flips, without branches
-  const bool odd = (q & 1u) != 0u;
-  const float a = odd ? s : c, b = odd ? c : s;
-  const uint32_t flip_cos = ((q + 1u) & 2u) << 30, flip_sin = (q & 2u) << 30;
-  return make_float2(__uint_as_float(__float_as_uint(a) ^ flip_cos),
-                     __uint_as_float(__float_as_uint(b) ^ flip_sin));
-}
-
 // ---------------------------------------------------------------------------
-// Table-driven forms for the Gaussian sampler.  Each workgroup builds the two
-// small tables in LDS from the functions above, so they hold the same bits
-// everywhere:
-//   turn[i] = (cos, sin) of 2 pi i / 256 (turn_cos_sin at i << 16)
-//   logt[i] = (R_i, L_i) for bin i of m in [1, 2) ([1 + i/128, 1 + (i+1)/128)):
-//             R_i = 1 / c_i (IEEE division, c_i the bin's midpoint) and
-//             L_i = -ln R_i, or -ln(2 R_i) with a factor 2 moved into the
-//             exponent for bins from 53 up (m >= 1.4140625); bin 0 uses R = 1
-//             and bin 127 R = 1/2, with L = 0, so logs near 1 do not cancel.
+// Gaussian sampler: one standard normal per Philox word x by inversion.
+// k = (x & 0xffffff) + 1 (exact in fp32), p = k 2^-24; the magnitude is the
+// half-normal quantile Phi^-1(1 - p/2), read from the table of cubics that
+// qd_archive_init builds on the host (QD_NORMAL_ROWS rows of (c0, c1, c2,
+// c3)): row = binary exponent of k times 16 plus its next four bits, taken
+// straight from the fp32 bits of k; u = its remaining 19 bits as an integer;
+// z = c0 + u (c1 + u (c2 + u c3)) by fma from the cubic term.  Bit 31 of x
+// is the sign (bits 24..30 are not used).  Ten VALU instructions and one
+// 16-byte LDS read per normal.  Every workgroup that draws normals stages the
+// table in LDS (6160 bytes).
 // ---------------------------------------------------------------------------
+constexpr int kNormalRows = QD_NORMAL_ROWS;
+
 struct Tables {
-  const float2* turn;   // [256]
-  const float2* logt;   // [128]
+  const float4* ntab;   // LDS copy of the table
 };
 
-__device__ __forceinline__ void build_tables(float2* turn, float2* logt, int tid, int nthreads) {
-  for (int i = tid; i < 256; i += nthreads) turn[i] = turn_cos_sin((uint32_t)i << 16);
-  for (int i = tid; i < 128; i += nthreads) {
-    float r = 1.0f, l = 0.0f;
-    if (i == 127) {
-      r = 0.5f;
-    } else if (i > 0) {
-      const float c = 1.0f + ((float)i + 0.5f) / 128.0f;
-      r = 1.0f / c;
-      l = -log_pos(i >= 53 ? r + r : r);
-    }
-    logt[i] = make_float2(r, l);
-  }
+__device__ __forceinline__ void stage_normal_table(float4* dst, const float4* src, int tid,
+                                                   int nthreads) {
+  for (int i = tid; i < kNormalRows; i += nthreads) dst[i] = src[i];
 }
 
-// cos and sin of 2 pi m / 2^24 from the turn table and the remainder
-// delta = (m & 0xffff) 2 pi 2^-24: sin delta ~ delta - delta^3/6,
-// cos delta ~ 1 - delta^2/2 + delta^4/24, angle-addition formulas.
-__device__ __forceinline__ float2 turn_tab(uint32_t m, const Tables& tb) {
-  const float2 t = tb.turn[m >> 16];
-  const float d = (float)(m & 0xffffu) * (kPi * 0x1p-23f);
-  const float d2 = d * d;
-  const float sd = fma32(d * d2, -1.0f / 6.0f, d);
-  const float cd = fma32(d2, fma32(d2, 1.0f / 24.0f, -0.5f), 1.0f);
-  return make_float2(fma32(t.x, cd, -(t.y * sd)), fma32(t.y, cd, t.x * sd));
-}
-
-// ln(k 2^-24), integer k in [1, 2^24]: k = 2^E m, bin i = top 7 fraction bits
-// of m, t = m R_i - 1 in one rounding, ln(m 2^-f) = L_i + t - t^2/2 + t^3/3
-// - t^4/4 (f = 1 for bins from 53 up), exponent E - 24 + f.
-__device__ __forceinline__ float log_k24(uint32_t k, const Tables& tb) {
+__device__ __forceinline__ float normal(uint32_t x, const Tables& tb) {
+  // k = (x & 0xffffff) + 1 as one 24-bit multiply-add (k * 1 + 1)
+  uint32_t k;
+  asm("v_mad_u32_u24 %0, %1, 1, 1" : "=v"(k) : "v"(x));
   const uint32_t b = __float_as_uint((float)k);
-  const uint32_t i = (b >> 16) & 0x7fu;
-  const int e = (int)(b >> 23) - (127 + 24) + (i >= 53u ? 1 : 0);
-  const float m = __uint_as_float((b & 0x7fffffu) | 0x3f800000u);
-  const float2 rl = tb.logt[i];
-  const float t = fma32(m, rl.x, -1.0f);
-  float q = fma32(t, -0.25f, 1.0f / 3.0f);
-  q = fma32(t, q, -0.5f);
-  const float lnm = rl.y + fma32(t * t, q, t);
-  const float fe = (float)e;
-  return fma32(fe, kLn2Hi, fma32(fe, kLn2Lo, lnm));
+  // row = (b >> 19) - 127 * 16: a bit-field extract (kept as one instruction:
+  // the compiler would rewrite it into a shift and a mask), then the scaled
+  // index and the bias go into one shift-and-add of the address
+  uint32_t e4;
+  asm("v_bfe_u32 %0, %1, 19, 12" : "=v"(e4) : "v"(b));
+  const float4 c = (tb.ntab - (127 << 4))[e4];
+  const float u = (float)(b & 0x7ffffu);
+  const float z = fma32(u, fma32(u, fma32(u, c.w, c.z), c.y), c.x);
+  return __uint_as_float(__float_as_uint(z) ^ (x & 0x80000000u));   // one v_bitop3
 }
-
-// Box-Muller radius sqrt(-2 ln u1), u1 = ((xa >> 8) + 1) 2^-24: with the IEEE
-// square root, and with the short sequence the kernels use.
-__device__ __forceinline__ float bm_radius_ieee(uint32_t xa, const Tables& tb) {
-  return __builtin_sqrtf(-2.0f * log_k24((xa >> 8) + 1u, tb));
-}
-__device__ __forceinline__ float bm_radius(uint32_t xa, const Tables& tb) {
-  return sqrt_normal(-2.0f * log_k24((xa >> 8) + 1u, tb));
-}
-
-// Two standard normals (Box-Muller) from two Philox words.
-__device__ __forceinline__ float2 gauss2(uint32_t xa, uint32_t xb, const Tables& tb) {
-  const float r = bm_radius(xa, tb);
-  const float2 cs = turn_tab(xb >> 8, tb);
-  return make_float2(r * cs.x, r * cs.y);
-}
-
 
 // sqrt(20) sin(pi x) up to sign (the sign may differ by (-1)^rint(x)):
 // r = x - rint(x) in [-1/2, 1/2] (exact), then r P(r^2), P the Taylor series

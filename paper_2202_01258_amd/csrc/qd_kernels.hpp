@@ -71,6 +71,7 @@ struct Params {
   uint8_t* off_bank;              // bank of parent 1 | bank of parent 2 << 1
   float* off_geno;                // [N_B][stride] or null
   double* stats;
+  const float4* ntab;   // Gaussian sampler table [QD_NORMAL_ROWS]
 };
 
 __device__ __forceinline__ float* geno_row(const Params& p, uint32_t bank, int cell) {
@@ -98,7 +99,7 @@ __device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, 
   q.c1 = pick(p.occ_list, x.x, nocc);
   q.c2 = pick(p.occ_list, x.y, nocc);
   q.tb = tb;
-  q.lambda = p.line_sigma * gauss2(x.z, x.w, tb).x;
+  q.lambda = p.line_sigma * normal(x.z, tb);
   const uint32_t b1 = p.arch_slot[q.c1], b2 = p.arch_slot[q.c2];
   q.banks = b1 | (b2 << 1);
   q.row1 = geno_row(p, b1, q.c1);
@@ -116,7 +117,7 @@ __device__ __forceinline__ Pair recorded_pair(const Params& p, uint32_t g, int j
   q.c2 = p.off_par[2 * j + 1];
   q.banks = p.off_bank[j];
   q.tb = tb;
-  q.lambda = p.line_sigma * gauss2(x.z, x.w, tb).x;
+  q.lambda = p.line_sigma * normal(x.z, tb);
   q.row1 = geno_row(p, q.banks & 1u, q.c1);
   q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
   return q;
@@ -141,13 +142,13 @@ __device__ __forceinline__ float4 make_genes(const Params& p, const Pair& q, uin
     const float4 t1 = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(q.row1) + off);
     const float4 t2 = *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(q.row2) + off);
     const uint4 x = philox((uint32_t)(base >> 2), (uint32_t)j, g, kTagIso, p.key);
-    const float2 e01 = gauss2(x.x, x.y, q.tb);
-    const float2 e23 = gauss2(x.z, x.w, q.tb);
+    const float e0 = normal(x.x, q.tb), e1 = normal(x.y, q.tb);
+    const float e2 = normal(x.z, q.tb), e3 = normal(x.w, q.tb);
     const float s1 = p.iso_sigma, l = q.lambda;
-    return make_float4(fma32(l, t2.x - t1.x, fma32(s1, e01.x, t1.x)),
-                       fma32(l, t2.y - t1.y, fma32(s1, e01.y, t1.y)),
-                       fma32(l, t2.z - t1.z, fma32(s1, e23.x, t1.z)),
-                       fma32(l, t2.w - t1.w, fma32(s1, e23.y, t1.w)));
+    return make_float4(fma32(l, t2.x - t1.x, fma32(s1, e0, t1.x)),
+                       fma32(l, t2.y - t1.y, fma32(s1, e1, t1.y)),
+                       fma32(l, t2.z - t1.z, fma32(s1, e2, t1.z)),
+                       fma32(l, t2.w - t1.w, fma32(s1, e3, t1.w)));
   }
 }
 
@@ -418,12 +419,12 @@ constexpr int kOffspringPerWave = 4;
 
 template <int TASK, bool GEN0, bool KEEP>
 __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
-  __shared__ float2 s_turn[256], s_logt[128];
+  __shared__ float4 s_ntab[kNormalRows];
   if (!GEN0) {
-    build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
+    stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, 256);
     __syncthreads();
   }
-  const Tables tb{s_turn, s_logt};
+  const Tables tb{s_ntab};
   const int lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kOffspringPerWave;
   if (j0 >= p.nb) return;
@@ -893,13 +894,13 @@ __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int first = blockIdx.x * kRegenCells;
   __shared__ uint64_t s_key[kRegenCells];
-  __shared__ float2 s_turn[256], s_logt[128];
+  __shared__ float4 s_ntab[kNormalRows];
   if (!stage_keys<kRegenCells>(p, first, s_key)) return;
   if (!GEN0) {
-    build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
+    stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, 256);
     __syncthreads();
   }
-  const Tables tb{s_turn, s_logt};
+  const Tables tb{s_ntab};
   const int wfirst = first + wave * kRegenCellsPerWave;
   const uint64_t* w_key = s_key + wave * kRegenCellsPerWave;
   for (int t = 0; t < kRegenCellsPerWave; ++t) {
@@ -1205,25 +1206,24 @@ __global__ __launch_bounds__(256) void k_cand_build(const Params p) {
 
 // Entry e of [A | B | s0] = 0.1 * normal (e mod 4) of block (e/4, 0, 0, ENV).
 __global__ void k_env(const Params p, int count) {
-  __shared__ float2 s_turn[256], s_logt[128];
-  build_tables(s_turn, s_logt, (int)threadIdx.x, (int)blockDim.x);
+  __shared__ float4 s_ntab[kNormalRows];
+  stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, (int)blockDim.x);
   __syncthreads();
-  const Tables tb{s_turn, s_logt};
+  const Tables tb{s_ntab};
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (4 * b >= count) return;
   const uint4 x = philox((uint32_t)b, 0u, 0u, kTagEnv, p.key);
-  const float2 z01 = gauss2(x.x, x.y, tb), z23 = gauss2(x.z, x.w, tb);
-  const float z[4] = {z01.x, z01.y, z23.x, z23.y};
+  const float z[4] = {normal(x.x, tb), normal(x.y, tb), normal(x.z, tb), normal(x.w, tb)};
   for (int k = 0; k < 4; ++k)
     if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
 }
 
-// Self-checks of the short division / square-root sequences against the IEEE
-// operations, over every input each one can receive: the Box-Muller radius
-// for all 2^24 inputs, tanh for all 2^32 fp32 bit patterns, sigmoid for all
-// fp32 values in [-1, 1].  Counts results that differ (both NaN = equal).
+// Self-checks of the short division sequences against the IEEE operations,
+// over every input each one can receive: tanh for all 2^32 fp32 bit patterns,
+// sigmoid for all fp32 values in [-1, 1].  Counts results that differ (both
+// NaN = equal).
 __global__ void k_zero_u64(unsigned long long* x) {
-  if (threadIdx.x < 3) x[threadIdx.x] = 0ull;
+  if (threadIdx.x < 2) x[threadIdx.x] = 0ull;
 }
 
 __device__ __forceinline__ bool same_bits(float a, float b) {
@@ -1231,25 +1231,16 @@ __device__ __forceinline__ bool same_bits(float a, float b) {
 }
 
 __global__ __launch_bounds__(256) void k_check_fast(unsigned long long* count) {
-  __shared__ float2 s_turn[256], s_logt[128];
-  build_tables(s_turn, s_logt, (int)threadIdx.x, 256);
-  __syncthreads();
-  const Tables tb{s_turn, s_logt};
   const uint64_t nthr = (uint64_t)gridDim.x * blockDim.x;
   const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  unsigned long long bad_r = 0, bad_t = 0, bad_s = 0;
-  for (uint64_t k = tid; k < (1ull << 24); k += nthr) {
-    const uint32_t xa = (uint32_t)k << 8;
-    bad_r += same_bits(bm_radius(xa, tb), bm_radius_ieee(xa, tb)) ? 0 : 1;
-  }
+  unsigned long long bad_t = 0, bad_s = 0;
   for (uint64_t k = tid; k < (1ull << 32); k += nthr) {
     const float x = __uint_as_float((uint32_t)k);
     bad_t += same_bits(tanh32<true>(x), tanh32<false>(x)) ? 0 : 1;
     if (__builtin_fabsf(x) <= 1.0f) bad_s += same_bits(sigmoid32<true>(x), sigmoid32<false>(x)) ? 0 : 1;
   }
-  if (bad_r) atomicAdd(count, bad_r);
-  if (bad_t) atomicAdd(count + 1, bad_t);
-  if (bad_s) atomicAdd(count + 2, bad_s);
+  if (bad_t) atomicAdd(count, bad_t);
+  if (bad_s) atomicAdd(count + 1, bad_s);
 }
 
 }  // namespace qd

@@ -253,7 +253,7 @@ __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, 
   __shared__ float s_rs[5][kRing + 1];
   __shared__ int s_fail;
 
-  __shared__ float2 s_turn[256], s_logt[128];
+  __shared__ float4 s_ntab[kNormalRows];
 
   const int o = threadIdx.x;
   const int j = blockIdx.x;
@@ -265,9 +265,9 @@ __global__ __launch_bounds__(H, H == 64 ? 3 : 2) void k_rollout(const Params p, 
       if (o == 0) record_empty_archive(p, j);
       return;
     }
-    build_tables(s_turn, s_logt, o, H);
+    stage_normal_table(s_ntab, p.ntab, o, H);
     __syncthreads();
-    q = select_pair(p, g, j, nocc, Tables{s_turn, s_logt});
+    q = select_pair(p, g, j, nocc, Tables{s_ntab});
   }
 
   // ---- prologue: this individual's genotype, straight into registers
@@ -404,13 +404,13 @@ __global__ __launch_bounds__(256) void k_regen_mlp(const Params p, uint32_t g) {
   const int first = blockIdx.x * kRegenCellsMlp;
   const int nblk = (p.n + 3) >> 2;
   __shared__ uint64_t s_key[kRegenCellsMlp];
-  __shared__ float2 s_turn[256], s_logt[128];
+  __shared__ float4 s_ntab[kNormalRows];
   if (!stage_keys<kRegenCellsMlp>(p, first, s_key)) return;
   if (!GEN0) {
-    build_tables(s_turn, s_logt, tid, 256);
+    stage_normal_table(s_ntab, p.ntab, tid, 256);
     __syncthreads();
   }
-  const Tables tb{s_turn, s_logt};
+  const Tables tb{s_ntab};
   for (int t = 0; t < kRegenCellsMlp; ++t) {
     const uint64_t key = s_key[t];
     if (!names_offspring(key)) continue;

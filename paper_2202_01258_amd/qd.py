@@ -15,8 +15,9 @@ from . import workloads as W
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqd.so")
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 CAND_SLOTS = 16
+NORMAL_ROWS = 385
 QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
     QD_ERR_UNSUPPORTED, QD_ERR_HIP = range(6)
 
@@ -24,7 +25,7 @@ QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
  BUF_CENTROIDS, BUF_BUCKET_START, BUF_BUCKET_ITEMS, BUF_CAND_COUNT, BUF_CAND_PTS,
  BUF_LLOYD_ACC, BUF_ENV, BUF_OCC_LIST, BUF_COUNTERS, BUF_OFF_PARENTS, BUF_OFF_FIT, BUF_OFF_DESC,
  BUF_OFF_CELL, BUF_OFF_WON, BUF_OFF_KEY, BUF_OFF_BANK, BUF_OFF_GENO, BUF_STATS,
- NUM_BUFFERS) = range(24)
+ BUF_NORMAL_TAB, NUM_BUFFERS) = range(25)
 
 (K_VARY_EVAL, K_ROLLOUT, K_INSERT, K_REGEN, K_SETUP, NUM_KERNELS) = range(6)
 KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
@@ -140,13 +141,13 @@ def layout_query(cfg: QdConfig) -> QdLayout:
 
 
 def check_fast_arith(device: str = "cuda:0") -> list:
-    """Mismatch counts of the short division / square-root sequences against
-    IEEE arithmetic: [Box-Muller radius (all 2^24 inputs), tanh (all 2^32),
-    sigmoid (|x| <= 1)], run on `device` and its current stream."""
+    """Mismatch counts of the short division sequences against IEEE
+    arithmetic: [tanh (all 2^32 inputs), sigmoid (|x| <= 1)], run on `device`
+    and its current stream."""
     import torch
     with torch.cuda.device(torch.device(device)):
-        scratch = torch.zeros(3, dtype=torch.int64, device=device)
-        out = (C.c_uint64 * 3)()
+        scratch = torch.zeros(2, dtype=torch.int64, device=device)
+        out = (C.c_uint64 * 2)()
         _check(lib().qd_check_fast_arith(C.c_void_p(scratch.data_ptr()),
                                          C.c_void_p(_stream_handle(None)), out),
                "qd_check_fast_arith")
@@ -263,6 +264,7 @@ class Archive:
             off_key=self.view(BUF_OFF_KEY, torch.int64, (nb,)),
             off_bank=self.view(BUF_OFF_BANK, torch.uint8, (nb,)),
             off_geno=self.view(BUF_OFF_GENO, torch.float32, (nb, st)),
+            normal_tab=self.view(BUF_NORMAL_TAB, torch.float32, (NORMAL_ROWS, 4)),
         )
 
     def snapshot(self) -> dict:
