@@ -204,6 +204,19 @@ qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_sta
 /* The layout the handle was created with. */
 qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
 
+/* Standard normals from the archive's Gaussian sampler, the one Algorithm 2's
+ * eps1 and eps2 come from in every generation (inversion through the table
+ * described at QD_NORMAL_ROWS): d_out[i] = the normal of the 32-bit word
+ * d_words[i] for i < count.  For checking the sampler on chosen words; the
+ * generations do not call it.  d_words (u32) and d_out (f32) are device
+ * memory owned by the caller, 4-byte aligned, each of count elements.
+ * QD_ERR_INVALID_ARG for a null handle, a null or misaligned pointer with
+ * count > 0, or count > 2^32; count 0 is a no-op.  Asynchronous on `stream`,
+ * which must be ordered after the stream qd_archive_init used (the table is
+ * written there). */
+qd_status qd_sample_normals(const qd_archive* h, const void* d_words, void* d_out, uint64_t count,
+                            void* stream);
+
 /* Selects the kernels whose launches carry a pair of HIP events on the launch
  * stream (hipExtLaunchKernelGGL: the runtime stamps them when the dispatch
  * begins and ends): bit k of kernel_mask is kernel QD_K_k (0 = no timing, the

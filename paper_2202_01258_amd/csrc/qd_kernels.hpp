@@ -1218,6 +1218,19 @@ __global__ void k_env(const Params p, int count) {
     if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
 }
 
+// The sampler on caller-given words (a grid-stride loop; i < count bounds
+// every access).
+__global__ __launch_bounds__(256) void k_sample_normals(const float4* ntab, const uint32_t* x,
+                                                        float* z, uint64_t count) {
+  __shared__ float4 s_ntab[kNormalRows];
+  stage_normal_table(s_ntab, ntab, (int)threadIdx.x, 256);
+  __syncthreads();
+  const Tables tb{s_ntab};
+  const uint64_t stride = (uint64_t)gridDim.x * 256u;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256u + threadIdx.x; i < count; i += stride)
+    z[i] = normal(x[i], tb);
+}
+
 // Self-checks of the short division sequences against the IEEE operations,
 // over every input each one can receive: tanh for all 2^32 fp32 bit patterns,
 // sigmoid for all fp32 values in [-1, 1].  Counts results that differ (both

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <array>
 #include <cmath>
 #include <cstring>
@@ -530,6 +531,19 @@ qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts) {
   }
   h->recs.clear();
   return st;
+}
+
+qd_status qd_sample_normals(const qd_archive* h, const void* d_words, void* d_out, uint64_t count,
+                            void* stream) {
+  if (!h || count > ((uint64_t)1 << 32)) return QD_ERR_INVALID_ARG;
+  if (count == 0) return QD_OK;
+  if (!d_words || !d_out || ((uintptr_t)d_words % 4) != 0 || ((uintptr_t)d_out % 4) != 0)
+    return QD_ERR_INVALID_ARG;
+  const unsigned grid = std::min(blocks_for(count, 256), 4096u);
+  hipLaunchKernelGGL(qd::k_sample_normals, dim3(grid), dim3(256), 0, (hipStream_t)stream, h->p.ntab,
+                     (const uint32_t*)d_words, (float*)d_out, count);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? QD_OK : hip_fail(e);
 }
 
 qd_status qd_check_fast_arith(void* d_scratch, void* stream, uint64_t* mismatches) {

@@ -33,7 +33,7 @@ KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
 # Every symbol include/qd.h declares.
 EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_generations",
            "qd_archive_stats",
-           "qd_archive_layout", "qd_set_kernel_timing", "qd_kernel_times",
+           "qd_archive_layout", "qd_sample_normals", "qd_set_kernel_timing", "qd_kernel_times",
            "qd_check_fast_arith", "qd_archive_destroy", "qd_status_str"]
 
 
@@ -92,6 +92,7 @@ def lib():
         L.qd_generations.argtypes = [P, C.c_uint32, C.c_uint32, P]
         L.qd_archive_stats.argtypes = [P, C.c_double, P, C.POINTER(QdStats)]
         L.qd_archive_layout.argtypes = [P, C.POINTER(QdLayout)]
+        L.qd_sample_normals.argtypes = [P, P, P, C.c_uint64, P]
         L.qd_set_kernel_timing.argtypes = [P, C.c_uint32]
         L.qd_kernel_times.argtypes = [P, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
         L.qd_check_fast_arith.argtypes = [P, P, C.POINTER(C.c_uint64)]
@@ -206,6 +207,22 @@ class Archive:
         """Generations first .. first + count - 1, enqueued by one library call."""
         _check(lib().qd_generations(self._h, first, count,
                                     C.c_void_p(_stream_handle(self.stream))), "qd_generations")
+
+    def sample_normals(self, words) -> "np.ndarray":
+        """The archive's Gaussian sampler applied to each 32-bit word (array-like
+        of uint32); runs on the archive's device and stream, returns numpy f32."""
+        import numpy as np
+        import torch
+        w = np.ascontiguousarray(np.asarray(words, dtype=np.uint32).ravel())
+        with torch.cuda.stream(self.stream):
+            d_w = torch.from_numpy(w.view(np.int32)).to(self.ws.device)
+            d_z = torch.empty(w.size, dtype=torch.float32, device=self.ws.device)
+            _check(lib().qd_sample_normals(self._h, C.c_void_p(d_w.data_ptr()),
+                                           C.c_void_p(d_z.data_ptr()), w.size,
+                                           C.c_void_p(_stream_handle(self.stream))),
+                   "qd_sample_normals")
+        self.stream.synchronize()
+        return d_z.cpu().numpy()
 
     def stats(self, offset: float = 0.0) -> dict:
         out = QdStats()

@@ -153,6 +153,12 @@ def test_workspace_checks_happen_before_gpu_work(lib):
     # argument checks come before the handle is used
     assert lib.qd_generations(fake, 0, 4, None) == Q.QD_ERR_INVALID_ARG
     assert lib.qd_generations(fake, 0xFFFFFFFF, 2, None) == Q.QD_ERR_INVALID_ARG
+    buf = C.c_void_p(1 << 41)
+    assert lib.qd_sample_normals(None, buf, buf, 4, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_sample_normals(fake, buf, buf, (1 << 32) + 1, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_sample_normals(fake, None, buf, 4, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_sample_normals(fake, buf, C.c_void_p((1 << 41) + 2), 4, None) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_sample_normals(fake, None, None, 0, None) == Q.QD_OK
     assert lib.qd_archive_destroy(None) == Q.QD_OK
     assert Q.status_str(Q.QD_ERR_WORKSPACE_TOO_SMALL) == "workspace too small"
 

@@ -428,6 +428,26 @@ def test_fast_division_equals_ieee_on_all_inputs():
     assert qd().check_fast_arith() == [0, 0]
 
 
+def test_sampler_bit_exact_on_every_magnitude_and_both_signs():
+    """All 2^24 magnitudes of the Gaussian sampler (every table row, including
+    the tail rows a generation almost never reaches), each with a random
+    choice of the unused bits 24..30 and both signs, against the oracle."""
+    w = W.workload("sphere_grid_b16384", batch=64)
+    a = qd().Archive(w)
+    k = np.arange(1 << 24, dtype=np.uint32)
+    mid = np.random.default_rng(11).integers(0, 128, size=k.size, dtype=np.uint32) << 24
+    for sign in (0, 0x80000000):
+        words = k | mid | np.uint32(sign)
+        say(f"sampler: 2^24 words, sign bit {sign >> 31}")
+        got = a.sample_normals(words)
+        want = O.normal(words)
+        np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+    # a count that is not a multiple of the workgroup size
+    words = np.random.default_rng(12).integers(0, 2**32, size=1001, dtype=np.uint64).astype(np.uint32)
+    np.testing.assert_array_equal(a.sample_normals(words).view(np.uint32),
+                                  O.normal(words).view(np.uint32))
+
+
 def test_normal_table_equals_the_oracle_table():
     """The Gaussian sampler's table that qd_archive_init builds on the host
     and copies into the workspace holds the oracle's bits (each side builds
