@@ -32,6 +32,9 @@ if ROOT not in sys.path:
 METRIC = "offspring evaluated+inserted/sec at 1 MI355X; % of peak HBM BW"
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 FP32_PEAK_TFLOPS = 157.3     # MI355X fp32 vector (dual-issue / packed) peak
+# VALU issue peak: 256 CUs x 4 SIMDs, one wave64 instruction per 2 cycles per
+# SIMD at 2.4 GHz -- the rate at which fma alone gives the fp32 figure above
+VALU_PEAK_PER_S = 256 * 4 * 2.4e9 / 2
 
 
 def log(msg: str):
@@ -151,6 +154,7 @@ def main():
     kernel_name = (f"k_rollout<{w['hid']}, false, false>" if w["task"] == 3
                    else f"k_vary_eval<{w['task']}, false, false>")
     traffic_file = os.path.join(ROOT, "profiles", f"k_{dominant}_{args.workload}_hbm_traffic.txt")
+    sq_file = os.path.join(ROOT, "profiles", f"k_{dominant}_{args.workload}_sq_counters.txt")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -218,8 +222,9 @@ def main():
         line["kernel_ms_per_step"] = {k: (v[0] / v[1] if v[1] else 0.0)
                                       for k, v in breakdown.items() if v[1]}
     if ktimes:
-        from paper_2202_01258_amd.rocprof_summary import recorded_traffic
+        from paper_2202_01258_amd.rocprof_summary import recorded_traffic, recorded_valu
         traffic = recorded_traffic(traffic_file, kernel_name)
+        valu_n = recorded_valu(sq_file, kernel_name)
         if w["task"] == 3:
             ms, cnt = ktimes["rollout"]
             avg = ms / cnt
@@ -238,6 +243,12 @@ def main():
                                 "frac": ach / HBM_PEAK_GBS, "traffic": traffic,
                                 "kernel_avg_us": avg * 1e3,
                                 "algorithmic_bytes_per_launch": bytes_model["vary_eval"] * nb}
+        # the same launch against the VALU issue limit, from the committed
+        # SQ_INSTS_VALU count of this kernel (null once the sources change)
+        line["roofline"]["valu"] = None if valu_n is None else {
+            "insts_per_launch": valu_n, "achieved": valu_n / (avg * 1e-3),
+            "peak": VALU_PEAK_PER_S, "unit": "wave64 VALU instructions/s",
+            "frac": valu_n / (avg * 1e-3) / VALU_PEAK_PER_S}
     if not args.no_cpu_baseline:
         log("bench: CPU baseline (oracle, one thread)")
         cb_w = dict(w)

@@ -18,6 +18,7 @@ import os
 import sqlite3
 
 TRAFFIC_TAG = "traffic_bytes_per_launch"
+VALU_TAG = "valu_insts_per_launch"
 
 
 def _open(db_path: str) -> sqlite3.Connection:
@@ -79,18 +80,28 @@ def sources_digest(kernel: str) -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(summary_path: str, kernel: str) -> float | None:
-    """Bytes per launch recorded for `kernel` in a --traffic summary, or None
-    when the file is absent or was taken on other kernel sources."""
+def _recorded(summary_path: str, tag: str, kernel: str) -> float | None:
     if not os.path.exists(summary_path):
         return None
     want = sources_digest(kernel)
     with open(summary_path) as fh:
         for line in fh:
             parts = line.split(maxsplit=3)
-            if len(parts) == 4 and parts[0] == TRAFFIC_TAG and parts[3].strip() == kernel:
+            if len(parts) == 4 and parts[0] == tag and parts[3].strip() == kernel:
                 return float(parts[1]) if parts[2] == want else None
     return None
+
+
+def recorded_traffic(summary_path: str, kernel: str) -> float | None:
+    """Bytes per launch recorded for `kernel` in a --traffic summary, or None
+    when the file is absent or was taken on other kernel sources."""
+    return _recorded(summary_path, TRAFFIC_TAG, kernel)
+
+
+def recorded_valu(summary_path: str, kernel: str) -> float | None:
+    """VALU instructions per launch recorded for `kernel` by --valu, or None
+    when the file is absent or was taken on other kernel sources."""
+    return _recorded(summary_path, VALU_TAG, kernel)
 
 
 def summary(db_path: str, top: int = 20) -> str:
@@ -147,18 +158,39 @@ def traffic(kernel: str, copy_fetch: str, copy_write: str, fetch: str, write: st
     ])
 
 
+def valu(kernel: str, db_path: str) -> str:
+    """SQ_INSTS_VALU of `kernel` summed over the counter instances of each
+    dispatch (a wave64 instruction counts once), averaged over dispatches."""
+    con = _open(db_path)
+    rows = con.execute("select dispatch_id, sum(counter_value) from pmc_events where "
+                       "counter_name = 'SQ_INSTS_VALU' and name like ? group by dispatch_id",
+                       (f"%{kernel}%",)).fetchall()
+    if not rows:
+        raise SystemExit(f"{db_path}: no SQ_INSTS_VALU rows for kernels like {kernel!r}")
+    per = [float(r[1]) for r in rows]
+    mean = sum(per) / len(per)
+    return "\n".join([
+        f"{kernel}: SQ_INSTS_VALU per dispatch (all instances) {mean:.0f}, over {len(per)} "
+        f"dispatches (min {min(per):.0f}, max {max(per):.0f})",
+        f"{VALU_TAG} {mean:.0f} {sources_digest(kernel)} {kernel}",
+    ])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("db", nargs="+")
     ap.add_argument("--top", type=int, default=20)
     ap.add_argument("--pmc", action="store_true")
     ap.add_argument("--traffic", metavar="KERNEL")
+    ap.add_argument("--valu", metavar="KERNEL")
     ap.add_argument("--copy-mib", type=int, default=256)
     a = ap.parse_args()
     if a.traffic:
         if len(a.db) != 4:
             raise SystemExit("--traffic takes copy_fetch.db copy_write.db fetch.db write.db")
         print(traffic(a.traffic, *a.db, a.copy_mib))
+    elif a.valu:
+        print(valu(a.valu, a.db[0]))
     else:
         print(pmc_summary(a.db[0], a.top) if a.pmc else summary(a.db[0], a.top))
 

@@ -1,5 +1,6 @@
-"""Host logic of the profile summaries: the recorded HBM traffic is used only
-while the sources its kernel is built from are unchanged."""
+"""Host logic of the profile summaries: the recorded HBM traffic and VALU
+instruction counts are used only while the sources their kernel is built from
+are unchanged."""
 import os
 
 from paper_2202_01258_amd import rocprof_summary as R
@@ -23,6 +24,17 @@ def test_recorded_traffic_matches_kernel_and_digest(tmp_path):
     assert R.recorded_traffic(str(f), ROLL) is None          # other sources
     assert R.recorded_traffic(str(f), "k_other") is None     # not recorded
     assert R.recorded_traffic(str(tmp_path / "absent.txt"), VARY) is None
+
+
+def test_recorded_valu_matches_kernel_and_digest(tmp_path):
+    f = tmp_path / "sq.txt"
+    f.write_text(f"{R.TRAFFIC_TAG} 5 {R.sources_digest(VARY)} {VARY}\n"
+                 f"{R.VALU_TAG} 49168434 {R.sources_digest(VARY)} {VARY}\n"
+                 f"{R.VALU_TAG} 7 {'f' * 64} {ROLL}\n")
+    assert R.recorded_valu(str(f), VARY) == 49168434.0   # its own tag, not traffic's
+    assert R.recorded_traffic(str(f), VARY) == 5.0
+    assert R.recorded_valu(str(f), ROLL) is None
+    assert R.recorded_valu(str(tmp_path / "absent.txt"), VARY) is None
 
 
 def test_committed_summaries_name_their_kernel():
