@@ -171,10 +171,10 @@ qd_status qd_layout_query(const qd_config* cfg, qd_layout* out);
  * point to its nearest centroid, each centroid that received points to their
  * mean) and the synthetic environment from their Philox streams, an empty
  * archive, N_B random genotypes evaluated and inserted.  The Gaussian sampler's
- * table (QD_BUF_NORMAL_TAB) is built on the host (once per process) and
- * copied into the workspace on `stream` ahead of that work; the host copy
- * lives until the process ends.  Asynchronous: returns once the work is
- * enqueued.  *out receives a host handle owned by the library (free it
+ * table (QD_BUF_NORMAL_TAB) is built on the host (once per process, about
+ * 10 ms the first time) and written into the workspace on `stream`, ahead of
+ * that work, by kernels that receive it as arguments.  Asynchronous: returns
+ * once the work is enqueued.  *out receives a host handle owned by the library (free it
  * with qd_archive_destroy).  The workspace must stay valid until then. */
 qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t workspace_bytes,
                           void* stream, qd_archive** out);

@@ -1218,6 +1218,18 @@ __global__ void k_env(const Params p, int count) {
     if (4 * b + k < count) p.env[4 * b + k] = 0.1f * z[k];
 }
 
+// The Gaussian sampler's table reaches the workspace as kernel arguments,
+// kTableChunk rows per launch, so that writing it needs no host buffer the
+// copy engine would have to read.
+constexpr int kTableChunk = 128;
+struct TableChunk {
+  float4 rows[kTableChunk];
+};
+__global__ void k_put_table(float4* dst, const TableChunk chunk, int first, int count) {
+  const int i = (int)threadIdx.x;
+  if (i < count) dst[first + i] = chunk.rows[i];
+}
+
 // The sampler on caller-given words (a grid-stride loop; i < count bounds
 // every access).
 __global__ __launch_bounds__(256) void k_sample_normals(const float4* ntab, const uint32_t* x,

@@ -427,8 +427,17 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
   hipStream_t s = (hipStream_t)stream;
   const qd::Params& p = h->p;
   {
-    const hipError_t e = hipMemcpyAsync((void*)p.ntab, normal_table().data(), 16 * QD_NORMAL_ROWS,
-                                        hipMemcpyHostToDevice, s);
+    // the sampler's table, as kernel arguments (no host copy to wait on)
+    const NormalTable& tab = normal_table();
+    for (int first = 0; first < QD_NORMAL_ROWS; first += qd::kTableChunk) {
+      const int count = std::min(qd::kTableChunk, QD_NORMAL_ROWS - first);
+      qd::TableChunk chunk;
+      std::memset(&chunk, 0, sizeof(chunk));
+      std::memcpy(&chunk.rows[0], &tab[4 * first], 16 * (size_t)count);
+      hipLaunchKernelGGL(qd::k_put_table, dim3(1), dim3(qd::kTableChunk), 0, s,
+                         (float4*)p.ntab, chunk, first, count);
+    }
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) {
       delete h;
       return hip_fail(e);
