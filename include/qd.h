@@ -204,6 +204,14 @@ qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_sta
 /* The layout the handle was created with. */
 qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
 
+/* Host only, no GPU work: copies the Gaussian sampler's table, the one
+ * qd_archive_init writes into QD_BUF_NORMAL_TAB, into out (QD_NORMAL_ROWS rows
+ * of 4 floats, c0 .. c3, row-major; host memory owned by the caller).  The
+ * table is built on the first call in the process (fp64 quantiles of the
+ * half-normal law interpolated at Chebyshev points, rounded once to fp32).
+ * QD_ERR_INVALID_ARG for a null pointer. */
+qd_status qd_normal_table(float* out);
+
 /* Standard normals from the archive's Gaussian sampler, the one Algorithm 2's
  * eps1 and eps2 come from in every generation (inversion through the table
  * described at QD_NORMAL_ROWS): d_out[i] = the normal of the 32-bit word

@@ -542,6 +542,13 @@ qd_status qd_kernel_times(qd_archive* h, double* ms, int32_t* counts) {
   return st;
 }
 
+qd_status qd_normal_table(float* out) {
+  if (!out) return QD_ERR_INVALID_ARG;
+  const NormalTable& tab = normal_table();
+  std::memcpy(out, tab.data(), sizeof(float) * tab.size());
+  return QD_OK;
+}
+
 qd_status qd_sample_normals(const qd_archive* h, const void* d_words, void* d_out, uint64_t count,
                             void* stream) {
   if (!h || count > ((uint64_t)1 << 32)) return QD_ERR_INVALID_ARG;

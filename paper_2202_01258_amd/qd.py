@@ -33,7 +33,8 @@ KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
 # Every symbol include/qd.h declares.
 EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_generations",
            "qd_archive_stats",
-           "qd_archive_layout", "qd_sample_normals", "qd_set_kernel_timing", "qd_kernel_times",
+           "qd_archive_layout", "qd_normal_table", "qd_sample_normals", "qd_set_kernel_timing",
+           "qd_kernel_times",
            "qd_check_fast_arith", "qd_archive_destroy", "qd_status_str"]
 
 
@@ -93,6 +94,7 @@ def lib():
         L.qd_archive_stats.argtypes = [P, C.c_double, P, C.POINTER(QdStats)]
         L.qd_archive_layout.argtypes = [P, C.POINTER(QdLayout)]
         L.qd_sample_normals.argtypes = [P, P, P, C.c_uint64, P]
+        L.qd_normal_table.argtypes = [C.POINTER(C.c_float)]
         L.qd_set_kernel_timing.argtypes = [P, C.c_uint32]
         L.qd_kernel_times.argtypes = [P, C.POINTER(C.c_double), C.POINTER(C.c_int32)]
         L.qd_check_fast_arith.argtypes = [P, P, C.POINTER(C.c_uint64)]
@@ -138,6 +140,15 @@ def make_config(w: dict, keep_offspring: bool = False) -> QdConfig:
 def layout_query(cfg: QdConfig) -> QdLayout:
     out = QdLayout()
     _check(lib().qd_layout_query(C.byref(cfg), C.byref(out)), "qd_layout_query")
+    return out
+
+
+def normal_table():
+    """The Gaussian sampler's table as the library builds it (host only):
+    numpy float32 [NORMAL_ROWS, 4]."""
+    import numpy as np
+    out = np.zeros((NORMAL_ROWS, 4), dtype=np.float32)
+    _check(lib().qd_normal_table(out.ctypes.data_as(C.POINTER(C.c_float))), "qd_normal_table")
     return out
 
 

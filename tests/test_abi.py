@@ -4,6 +4,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2202_01258_amd import qd as Q
@@ -161,6 +162,17 @@ def test_workspace_checks_happen_before_gpu_work(lib):
     assert lib.qd_sample_normals(fake, None, None, 0, None) == Q.QD_OK
     assert lib.qd_archive_destroy(None) == Q.QD_OK
     assert Q.status_str(Q.QD_ERR_WORKSPACE_TOO_SMALL) == "workspace too small"
+
+
+def test_library_table_equals_the_oracle_table(lib):
+    """The Gaussian sampler's table the library builds on the host (its own
+    fp64 code) holds the oracle's bits; no GPU needed."""
+    from oracle import oracle as O
+    got = Q.normal_table()
+    want = O.normal_table()
+    assert got.shape == want.shape == (Q.NORMAL_ROWS, 4)
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+    assert lib.qd_normal_table(None) == Q.QD_ERR_INVALID_ARG
 
 
 def test_product_path_refuses_without_gpu(lib):
