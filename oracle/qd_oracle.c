@@ -519,8 +519,7 @@ void or_free(or_state* s) {
 
 /* Centroids: coordinate k of centroid c is the 24-bit uniform of word k of
  * block (c, 0, 0, CENTROID).  Environment: entry e of [A | B | s0] is 0.1
- * times normal number e mod 4 of block (e/4, 0, 0, ENV), the block's words
- * giving two Box-Muller pairs. */
+ * times the normal of word e mod 4 of block (e/4, 0, 0, ENV). */
 /* Centroidal Voronoi tessellation by Lloyd's algorithm (the CVT the paper
  * cites for its tessellations): cvt_iters times, every one of cvt_samples
  * uniform points of [0,1]^D (point i, coordinate k = U24 of word k of block

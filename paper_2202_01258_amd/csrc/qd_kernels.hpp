@@ -89,7 +89,7 @@ struct Pair {
   float lambda;
   int c1, c2;
   uint32_t banks;
-  Tables tb;                      // the workgroup's sampler tables (LDS)
+  Tables tb;                      // the workgroup's sampler table (LDS)
 };
 
 __device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, int nocc,
