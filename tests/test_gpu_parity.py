@@ -250,6 +250,38 @@ def test_generations_in_one_call_equal_single_calls(name, kw):
         np.testing.assert_array_equal(la[k], lb[k], err_msg=k)
 
 
+def check_driven_generation(a, o, w, g):
+    """Runs generation g on the GPU from its current archive and checks it
+    against the oracle started from the same archive: every offspring's cell
+    and the whole insertion, sampled offspring, and the winners' rows."""
+    pre = a.snapshot()
+    a.generation(g)
+    gb = a.last_batch()
+    o.set_archive(pre["geno"], pre["fit"], pre["desc"], pre["occ"])
+    rng = np.random.default_rng(g)
+    for j in np.concatenate([[0, 1, w["batch"] - 1], rng.integers(0, w["batch"], 12)]):
+        geno, fit, desc, par = o.offspring(g, int(j))
+        np.testing.assert_array_equal(par, gb["parents"][j])
+        assert gb["fit"][j] == fit
+        np.testing.assert_array_equal(gb["desc"][j], desc)
+    cell, won = o.insert_driven(gb["fit"], gb["desc"])
+    np.testing.assert_array_equal(gb["cell"], cell)
+    np.testing.assert_array_equal(gb["won"], won)
+    post = a.snapshot()
+    oa = o.archive()
+    np.testing.assert_array_equal(post["occ"], oa["occ"])
+    filled = oa["occ"] == 1
+    np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
+    np.testing.assert_array_equal(post["desc"][filled], oa["desc"][filled])
+    # winners' rows: regenerated on the GPU, recomputed here
+    for j in np.nonzero(won)[0][:8]:
+        geno, fit, desc, _ = o.offspring(g, int(j))
+        np.testing.assert_array_equal(post["geno"][gb["cell"][j]], geno)
+    # the tolerance the method states, for the record
+    assert rel_err(post["fit"][filled], oa["fit"][filled], 1e-6) <= 1e-5
+    return int(won.sum())
+
+
 @pytest.mark.parametrize("batch", [65536, 131072])
 def test_full_size_rastrigin_projection_sampled(batch):
     """n = 1000, CVT 10^4 at N_B = 65536 (the benchmark's launch configuration)
@@ -264,31 +296,22 @@ def test_full_size_rastrigin_projection_sampled(batch):
     np.testing.assert_array_equal(a.views()["centroids"].cpu().numpy(), o.centroids())
     for g in (1, 2):
         say(f"full size rastrigin projection: generation {g}")
-        pre = a.snapshot()
-        a.generation(g)
-        gb = a.last_batch()
-        o.set_archive(pre["geno"], pre["fit"], pre["desc"], pre["occ"])
-        rng = np.random.default_rng(g)
-        for j in np.concatenate([[0, 1, w["batch"] - 1], rng.integers(0, w["batch"], 12)]):
-            geno, fit, desc, par = o.offspring(g, int(j))
-            np.testing.assert_array_equal(par, gb["parents"][j])
-            assert gb["fit"][j] == fit
-            np.testing.assert_array_equal(gb["desc"][j], desc)
-        cell, won = o.insert_driven(gb["fit"], gb["desc"])
-        np.testing.assert_array_equal(gb["cell"], cell)
-        np.testing.assert_array_equal(gb["won"], won)
-        post = a.snapshot()
-        oa = o.archive()
-        np.testing.assert_array_equal(post["occ"], oa["occ"])
-        filled = oa["occ"] == 1
-        np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
-        np.testing.assert_array_equal(post["desc"][filled], oa["desc"][filled])
-        # winners' rows: regenerated on the GPU, recomputed here
-        for j in np.nonzero(won)[0][:8]:
-            geno, fit, desc, _ = o.offspring(g, int(j))
-            np.testing.assert_array_equal(post["geno"][gb["cell"][j]], geno)
-        # the tolerance the method states, for the record
-        assert rel_err(post["fit"][filled], oa["fit"][filled], 1e-6) <= 1e-5
+        check_driven_generation(a, o, w, g)
+
+
+def test_benchmark_configuration_at_generation_200_driven():
+    """The benchmark configuration run on the GPU alone for the paper's 199
+    generations, then generation 200 checked against the oracle from the
+    archive the GPU reached: parity deep into the run that is timed."""
+    w = W.workload("rastrigin_proj_cvt_b65536")
+    say("benchmark configuration: init, 199 free-running generations")
+    a = qd().Archive(w)
+    a.generations(1, 199)
+    o = O.Oracle(w)
+    o.setup()
+    say("benchmark configuration: generation 200, driven")
+    check_driven_generation(a, o, w, 200)
+    assert a.stats()["num_occupied"] >= 1
 
 
 MLP_SMALL = {
@@ -379,6 +402,43 @@ def test_mlp_full_size_sampled(name, batch, samples):
     np.testing.assert_array_equal(post["occ"], oa["occ"])
     filled = oa["occ"] == 1
     np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
+
+
+def test_policy_configuration_at_generation_100_driven():
+    """The 27-64-64-8 policy configuration (T = 250, N_B = 8192) run on the GPU
+    alone for the paper's 99 generations, then generation 100 checked from
+    the archive the GPU reached: sampled rollouts, every cell and the
+    insertion, and the winners' regenerated rows."""
+    w = W.workload("mlp64_cvt_b8192")
+    say("policy configuration: init, 99 free-running generations")
+    a = qd().Archive(w)
+    a.generations(1, 99)
+    o = O.Oracle(w)
+    o.setup()
+    g = 100
+    say("policy configuration: generation 100, driven")
+    pre = a.snapshot()
+    a.generation(g)
+    gb = a.last_batch()
+    o.set_archive(pre["geno"], pre["fit"], pre["desc"], pre["occ"])
+    rng = np.random.default_rng(g)
+    for j in np.concatenate([[0, w["batch"] - 1], rng.integers(0, w["batch"], 4)]):
+        say(f"  oracle rollout j={j}")
+        geno, fit, desc, par = o.offspring(g, int(j))
+        np.testing.assert_array_equal(par, gb["parents"][j])
+        assert gb["fit"][j] == fit, (j, gb["fit"][j], fit)
+        np.testing.assert_array_equal(gb["desc"][j], desc)
+    cell, won = o.insert_driven(gb["fit"], gb["desc"])
+    np.testing.assert_array_equal(gb["cell"], cell)
+    np.testing.assert_array_equal(gb["won"], won)
+    post, oa = a.snapshot(), o.archive()
+    np.testing.assert_array_equal(post["occ"], oa["occ"])
+    filled = oa["occ"] == 1
+    np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
+    np.testing.assert_array_equal(post["desc"][filled], oa["desc"][filled])
+    for j in np.nonzero(won)[0][:4]:
+        geno, _, _, _ = o.offspring(g, int(j))
+        np.testing.assert_array_equal(post["geno"][gb["cell"][j]], geno)
 
 
 @pytest.mark.parametrize("kw", [dict(batch=1), dict(n=2, batch=5), dict(n=101, batch=9),
