@@ -404,19 +404,21 @@ def test_mlp_full_size_sampled(name, batch, samples):
     np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
 
 
-def test_policy_configuration_at_generation_100_driven():
-    """The 27-64-64-8 policy configuration (T = 250, N_B = 8192) run on the GPU
-    alone for the paper's 99 generations, then generation 100 checked from
-    the archive the GPU reached: sampled rollouts, every cell and the
-    insertion, and the winners' regenerated rows."""
-    w = W.workload("mlp64_cvt_b8192")
-    say("policy configuration: init, 99 free-running generations")
+@pytest.mark.parametrize("name,G", [("mlp64_cvt_b8192", 100), ("mlp128_cvt_b65536", 50)])
+def test_policy_configuration_at_last_generation_driven(name, G):
+    """A policy configuration (27-64-64-8, T = 250, N_B = 8192; 27-128-128-8,
+    T = 1000, N_B = 65536) run on the GPU alone for the paper's G - 1
+    generations, then generation G checked from the archive the GPU reached:
+    sampled rollouts, every cell and the insertion, and the winners'
+    regenerated rows."""
+    w = W.workload(name)
+    say(f"policy configuration {name}: init, {G - 1} free-running generations")
     a = qd().Archive(w)
-    a.generations(1, 99)
+    a.generations(1, G - 1)
     o = O.Oracle(w)
     o.setup()
-    g = 100
-    say("policy configuration: generation 100, driven")
+    g = G
+    say(f"policy configuration {name}: generation {G}, driven")
     pre = a.snapshot()
     a.generation(g)
     gb = a.last_batch()
