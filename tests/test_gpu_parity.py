@@ -63,6 +63,10 @@ SMALL = {
     # the same on a Lloyd CVT (centroids moved by three Lloyd iterations)
     "proj_spread_lloyd": dict(n=8, batch=2000, C=500, init_lo=-5.12, init_hi=5.12, seed=4,
                               cvt_samples=20000, cvt_iters=3),
+    # a short genotype (two offspring per wave) on a CVT, descriptors over the
+    # whole box: the (theta_0, theta_1) descriptor through the candidate lists
+    "sphere_cvt_spread": dict(tess=W.CVT, C=500, grid=(0, 0), batch=300, init_lo=-5.12,
+                              init_hi=5.12, seed=6),
 }
 
 
@@ -71,6 +75,8 @@ def small_workload(name):
         return W.workload("rastrigin_grid_b128", n=257, batch=77, seed=5)
     if name in ("proj_spread_cvt", "proj_spread_lloyd"):
         return W.workload("rastrigin_proj_cvt_b65536", **SMALL[name])
+    if name == "sphere_cvt_spread":
+        return W.workload("sphere_grid_b16384", **SMALL[name])
     return W.workload(name, **SMALL[name])
 
 
@@ -335,6 +341,11 @@ MLP_SMALL = {
     # smallest one searched by rings instead
     "mlp64_cvt_2048_lds": ("mlp64_cvt_b8192", dict(batch=40, T=8, C=2048)),
     "mlp64_cvt_2049_rings": ("mlp64_cvt_b8192", dict(batch=40, T=8, C=2049)),
+    # policies on a 4-D grid of 5^4 cells (grid insertion with D = 4); the
+    # box is narrowed around 0.5, where these descriptors lie, so the batch
+    # spreads over 17 cells and reaches 85 in three generations
+    "mlp64_grid_4d": ("mlp64_cvt_b8192", dict(batch=40, T=20, tess=W.GRID, grid=(5, 5, 5, 5),
+                                              C=625, lo=(0.498,) * 4, hi=(0.502,) * 4)),
 }
 
 
