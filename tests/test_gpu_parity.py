@@ -195,6 +195,10 @@ def test_generations_driven_bit_exact(name):
     ("sphere_grid_b16384", {}, 500),                         # the full configuration
     ("rastrigin_proj_cvt_b65536", dict(batch=2048), 12),
     ("rastrigin_proj_cvt_b65536", {}, 3),                    # the benchmark configuration
+    # first batch over the whole box: thousands of new cells and winners in
+    # every early generation (regeneration and compaction at full load)
+    ("rastrigin_grid_b128", dict(batch=4096, init_lo=-5.12, init_hi=5.12, seed=2), 40),
+    ("sphere_grid_b16384", dict(batch=4096, init_lo=-5.12, init_hi=5.12, seed=3), 10),
 ])
 def test_end_to_end_qd_score(name, kw, G):
     w = W.workload(name, **kw)
