@@ -15,7 +15,12 @@ device synchronisation, with nothing else on the stream.  The paper's eval/s
 steps with a HIP event after each.  The roofline object is for the dominant
 kernel, whose per-launch duration comes from start/stop HIP events attached to
 each of its launches on its stream (hipExtLaunchKernelGGL) over a third run of
-K steps.
+K steps.  Beside the bound the metric names (HBM bytes of the byte model, or
+fp32 flops for policies) it carries two figures taken from the committed
+rocprofv3 summaries under profiles/, each only while the kernel's sources
+still hash to the value recorded with it: `traffic`, the measured HBM bytes
+per launch, and `valu`, the kernel's VALU instructions per launch over the
+same duration against one wave64 instruction per 2 cycles per SIMD.
 """
 from __future__ import annotations
 
