@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define QD_ABI_VERSION 5u
+#define QD_ABI_VERSION 6u
 
 /* Candidate slots per fine bucket of a two-dimensional CVT (see QD_BUF_CAND_*). */
 #define QD_CAND_SLOTS 16
@@ -95,6 +95,13 @@ typedef struct {
                           /*   state before its failure gets a NaN objective and  */
                           /*   descriptor 0.  Must be 0 for the test functions.  */
   float death_below;      /*   the failure threshold (any non-NaN value)          */
+  int32_t init_mode;      /* test functions' first batch: 0 every gene U[init_lo, */
+                          /*   init_hi); 1 ("spread") individual j also draws one  */
+                          /*   level per genotype half h (genes [0, n/2) and      */
+                          /*   [n/2, n)), desc_lo[h] + U (desc_hi[h] - desc_lo[h]),*/
+                          /*   added to every gene of that half, so the first     */
+                          /*   batch covers the descriptor box even where a       */
+                          /*   descriptor averages many genes.  Must be 0 for MLP. */
   uint64_t seed;          /* key of every Philox4x32-10 stream                    */
 } qd_config;
 

@@ -1,7 +1,9 @@
 """Builds the CPU oracle (test infrastructure only) into oracle/liboracle.so.
 
 The oracle is plain C compiled without floating-point contraction or fast-math
-so that every fused multiply-add in it is an explicit fmaf() call.
+so that every fused multiply-add in it is an explicit fmaf() call.  OpenMP
+runs its per-offspring loops on several threads; build(openmp=False, path=...)
+makes the single-threaded build of the same source (the pragmas are ignored).
 """
 import os
 import subprocess
@@ -13,15 +15,15 @@ FLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-sh
          "-Wall", "-Wextra", "-Wno-unused-parameter"]
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, openmp: bool = True, path: str = LIB) -> str:
     src = os.path.join(HERE, "qd_oracle.c")
-    tmp = LIB + ".tmp"
-    cmd = ["gcc", *FLAGS, src, "-o", tmp, "-lm"]
+    tmp = path + ".tmp"
+    cmd = ["gcc", *FLAGS, *(["-fopenmp"] if openmp else []), src, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, path)
+    return path
 
 
 if __name__ == "__main__":

@@ -26,20 +26,23 @@ class OrConfig(C.Structure):
         ("init_lo", C.c_float), ("init_hi", C.c_float),
         ("obs", C.c_int32), ("hid", C.c_int32), ("act", C.c_int32), ("T", C.c_int32),
         ("cvt_samples", C.c_int32), ("cvt_iters", C.c_int32),
-        ("death_mode", C.c_int32), ("death_below", C.c_float), ("seed", C.c_uint64),
+        ("death_mode", C.c_int32), ("death_below", C.c_float), ("init_mode", C.c_int32),
+        ("seed", C.c_uint64),
     ]
 
 
 _lib = None
 
 
-def lib():
+def lib(path: str | None = None):
+    """The oracle library (built on first use).  With `path`, a separately
+    built copy of it (e.g. the single-threaded build), loaded afresh."""
     global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
+    if path is not None or _lib is None:
+        if path is None and not os.path.exists(LIB_PATH):
             from oracle import build as _b
             _b.build()
-        L = C.CDLL(LIB_PATH)
+        L = C.CDLL(path or LIB_PATH)
         P = C.c_void_p
         f32p, u32p, i32p, u8p = (C.POINTER(C.c_float), C.POINTER(C.c_uint32),
                                  C.POINTER(C.c_int32), C.POINTER(C.c_uint8))
@@ -73,6 +76,9 @@ def lib():
             "or_init": (C.c_int32, [P]),
             "or_generation": (C.c_int32, [P, C.c_uint32]),
             "or_offspring": (C.c_int32, [P, C.c_uint32, C.c_int32, f32p, f32p, f32p, i32p]),
+            "or_offspring_many": (C.c_int32, [P, C.c_uint32, i32p, C.c_int32, f32p, f32p,
+                                              i32p]),
+            "or_set_threads": (C.c_int32, [C.c_int32]),
             "or_insert_driven": (C.c_int32, [P, f32p, f32p, f32p, C.c_int32, i32p, u8p]),
             "or_stats": (None, [P, C.c_double, C.POINTER(C.c_double)]),
             "or_archive_geno": (f32p, [P]), "or_archive_fit": (f32p, [P]),
@@ -86,8 +92,15 @@ def lib():
             fn = getattr(L, name)
             fn.restype = res
             fn.argtypes = args
+        if path is not None:
+            return L
         _lib = L
     return _lib
+
+
+def set_threads(n: int = 0) -> int:
+    """Threads of the oracle's per-offspring loops (0: keep); returns the count."""
+    return int(lib().or_set_threads(n))
 
 
 def _ptr(a: np.ndarray, ctype):
@@ -107,6 +120,7 @@ def make_config(w: dict) -> OrConfig:
     c.obs, c.hid, c.act, c.T = w["obs"], w["hid"], w["act"], w["T"]
     c.cvt_samples, c.cvt_iters = w.get("cvt_samples", 0), w.get("cvt_iters", 0)
     c.death_mode, c.death_below = w.get("death_mode", 0), w.get("death_below", 0.0)
+    c.init_mode = w.get("init_mode", 0)
     c.seed = w["seed"]
     return c
 
@@ -219,12 +233,13 @@ def key(f: float, j: int, batch: int) -> int:
 
 # ---------------------------------------------------------------- the run
 class Oracle:
-    """One oracle archive with its configuration (Algorithm 1 state)."""
+    """One oracle archive with its configuration (Algorithm 1 state).  `path`
+    selects a separately built copy of the oracle library."""
 
-    def __init__(self, w: dict):
+    def __init__(self, w: dict, path: str | None = None):
         self.w = dict(w)
         self.cfg = make_config(w)
-        L = lib()
+        self._L = L = lib(path) if path is not None else lib()
         self.n = L.or_genotype_len(C.byref(self.cfg))
         self.env_len = L.or_env_len(C.byref(self.cfg))
         self._s = L.or_new(C.byref(self.cfg), 0)
@@ -233,18 +248,18 @@ class Oracle:
     def __del__(self):
         s = getattr(self, "_s", None)
         if s:
-            lib().or_free(s)
+            self._L.or_free(s)
             self._s = None
 
     # -- steps
     def setup(self):
-        lib().or_setup(self._s)
+        self._L.or_setup(self._s)
 
     def init(self):
-        return lib().or_init(self._s)
+        return self._L.or_init(self._s)
 
     def generation(self, g: int):
-        rc = lib().or_generation(self._s, g)
+        rc = self._L.or_generation(self._s, g)
         if rc != 0:
             raise RuntimeError("oracle generation failed (empty archive)")
 
@@ -253,11 +268,25 @@ class Oracle:
         fit = np.zeros(1, np.float32)
         desc = np.zeros(4, np.float32)
         par = np.zeros(2, np.int32)
-        rc = lib().or_offspring(self._s, g, j, _ptr(geno, C.c_float), _ptr(fit, C.c_float),
+        rc = self._L.or_offspring(self._s, g, j, _ptr(geno, C.c_float), _ptr(fit, C.c_float),
                                 _ptr(desc, C.c_float), _ptr(par, C.c_int32))
         if rc != 0:
             raise RuntimeError("oracle offspring failed (empty archive)")
         return geno, fit[0], desc[: self.D].copy(), par
+
+    def offspring_many(self, g: int, js):
+        """Objectives, descriptors and parents of offspring js of generation g
+        from the archive as it stands (parallel over js; nothing inserted)."""
+        js = np.ascontiguousarray(np.asarray(js, dtype=np.int32).ravel())
+        fit = np.zeros(js.size, np.float32)
+        desc = np.zeros((js.size, self.D), np.float32)
+        par = np.zeros((js.size, 2), np.int32)
+        rc = self._L.or_offspring_many(self._s, g, _ptr(js, C.c_int32), js.size,
+                                       _ptr(fit, C.c_float), _ptr(desc, C.c_float),
+                                       _ptr(par, C.c_int32))
+        if rc != 0:
+            raise RuntimeError("oracle offspring failed (empty archive)")
+        return fit, desc, par
 
     def insert_driven(self, fit, desc, geno=None):
         fit = np.ascontiguousarray(np.asarray(fit, dtype=np.float32))
@@ -269,18 +298,18 @@ class Oracle:
         if geno is not None:
             geno = np.ascontiguousarray(np.asarray(geno, dtype=np.float32).reshape(nb, self.n))
             gp = _ptr(geno, C.c_float)
-        lib().or_insert_driven(self._s, _ptr(fit, C.c_float), _ptr(desc, C.c_float), gp, nb,
+        self._L.or_insert_driven(self._s, _ptr(fit, C.c_float), _ptr(desc, C.c_float), gp, nb,
                                _ptr(cell, C.c_int32), _ptr(won, C.c_uint8))
         return cell, won
 
     def stats(self, offset: float = 0.0):
         out = (C.c_double * 3)()
-        lib().or_stats(self._s, offset, out)
+        self._L.or_stats(self._s, offset, out)
         return dict(qd_score=out[0], coverage=int(out[1]), best=out[2])
 
     # -- views (copies)
     def _arr(self, fn, ctype, count, shape):
-        p = getattr(lib(), fn)(self._s)
+        p = getattr(self._L, fn)(self._s)
         return np.ctypeslib.as_array(C.cast(p, C.POINTER(ctype)), shape=(count,)).reshape(
             shape).copy()
 
@@ -299,7 +328,7 @@ class Oracle:
                                     ("or_archive_fit", fit, C.c_float, C_),
                                     ("or_archive_desc", desc, C.c_float, C_ * D),
                                     ("or_archive_occ", occ, C.c_uint8, C_)):
-            p = getattr(lib(), fn)(self._s)
+            p = getattr(self._L, fn)(self._s)
             dst = np.ctypeslib.as_array(C.cast(p, C.POINTER(ctype)), shape=(cnt,))
             dst[:] = np.asarray(arr).reshape(-1)
 

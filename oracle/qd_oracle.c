@@ -1,7 +1,11 @@
 /*
- * qd_oracle.c -- plain, slow, single-threaded CPU oracle of massively-parallel
- * MAP-Elites ("Accelerated Quality-Diversity through Massive Parallelism",
- * Lim, Allard, Grillotti, Cully; arXiv 2202.01258).
+ * qd_oracle.c -- plain, slow CPU oracle of massively-parallel MAP-Elites
+ * ("Accelerated Quality-Diversity through Massive Parallelism", Lim, Allard,
+ * Grillotti, Cully; arXiv 2202.01258).  The per-offspring loops (select,
+ * vary, evaluate, map to a cell) may run on several threads through OpenMP:
+ * each offspring depends only on the archive before the generation, so the
+ * results do not depend on the thread count.  Insertion is Algorithm 1's
+ * sequential loop and always runs in one thread.
  *
  * TEST INFRASTRUCTURE ONLY.  It exists so that the HIP library can be checked
  * against something written straight from the paper.  Only the test-suite, the
@@ -39,6 +43,9 @@
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 /* ------------------------------------------------------------------------ */
 /* Bits                                                                      */
@@ -72,7 +79,7 @@ void or_philox(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
 
 /* Stream tags (fourth counter word).  Counter = (item, individual, generation, tag). */
 enum { TAG_INIT = 0, TAG_SELECT = 1, TAG_ISO = 2, TAG_CENTROID = 3, TAG_ENV = 4,
-       TAG_CVT_SAMPLE = 5 };
+       TAG_CVT_SAMPLE = 5, TAG_INIT_LEVEL = 6 };
 
 static void draw(const or_state* s, uint32_t item, uint32_t indiv, uint32_t gen,
                  uint32_t tag, uint32_t out[4]);
@@ -487,6 +494,10 @@ static void draw(const or_state* s, uint32_t item, uint32_t indiv, uint32_t gen,
 }
 
 or_state* or_new(const or_config* cfg, int32_t keep_offspring) {
+  /* the lazily built tables are built here, before any parallel loop reads them */
+  float coef[6];
+  build_normal_table();
+  or_rsin_coef(coef);
   or_state* s = (or_state*)calloc(1, sizeof(or_state));
   s->cfg = *cfg;
   s->n = or_genotype_len(cfg);
@@ -574,18 +585,30 @@ void or_setup(or_state* s) {
   }
 }
 
-/* Random first batch (Algorithm 1, first iteration).  Test functions: gene
- * i = lo + U * (hi - lo).  Policies: Glorot-uniform weights in
+/* Random first batch (Algorithm 1, first iteration: random solutions).
+ * Test functions: gene i = lo + U * (hi - lo); with init_mode 1 individual j
+ * also draws one level per genotype half h (genes [0, n/2) and [n/2, n)),
+ * uniform over descriptor dimension h's box, lo_h + U (hi_h - lo_h) from word
+ * h of block (0, j, 0, INIT_LEVEL), and adds it to every gene of that half,
+ * so that the first batch covers the descriptor box even where a descriptor
+ * averages many genes.  Policies: Glorot-uniform weights in
  * [-a, a), a = sqrt(6 / (fan_in + fan_out)), zero biases. */
 static void init_genotype(const or_state* s, int32_t j, float* out) {
   const or_config* c = &s->cfg;
   int32_t n = s->n;
   uint32_t x[4] = {0, 0, 0, 0};
+  float level[2] = {0.0f, 0.0f};
+  if (c->task != OR_MLP && c->init_mode == 1) {
+    uint32_t y[4];
+    draw(s, 0, (uint32_t)j, 0, TAG_INIT_LEVEL, y);
+    for (int h = 0; h < 2; ++h) level[h] = fmaf(or_u24(y[h]), c->hi[h] - c->lo[h], c->lo[h]);
+  }
   for (int32_t i = 0; i < n; ++i) {
     if ((i & 3) == 0) draw(s, (uint32_t)(i >> 2), (uint32_t)j, 0, TAG_INIT, x);
     float u = or_u24(x[i & 3]);
     if (c->task != OR_MLP) {
       out[i] = fmaf(u, c->init_hi - c->init_lo, c->init_lo);
+      if (c->init_mode == 1) out[i] = level[i < n / 2 ? 0 : 1] + out[i];
     } else {
       int32_t o = c->obs, h = c->hid, a = c->act;
       int32_t e1 = h * o, e2 = e1 + h, e3 = e2 + h * h, e4 = e3 + h, e5 = e4 + a * h;
@@ -693,6 +716,8 @@ int32_t or_init(or_state* s) {
   or_setup(s);
   int32_t n = s->n, D = c->D, nb = c->batch;
   ensure_offspring_storage(s);
+  /* the offspring are independent of one another: evaluated in parallel */
+#pragma omp parallel for schedule(dynamic, 8)
   for (int32_t j = 0; j < nb; ++j) {
     float* x = s->off_geno + (size_t)j * n;
     init_genotype(s, j, x);
@@ -711,6 +736,9 @@ int32_t or_generation(or_state* s, uint32_t g) {
   int32_t nocc = build_occ_list(s);
   if (nocc == 0) return -1;
   ensure_offspring_storage(s);
+  /* select, vary, evaluate and map each offspring (independent of one
+   * another, in parallel); then Algorithm 1's insertion loop in batch order */
+#pragma omp parallel for schedule(dynamic, 8)
   for (int32_t j = 0; j < nb; ++j) {
     float* x = s->off_geno + (size_t)j * n;
     make_offspring(s, g, j, nocc, x, s->parents + 2 * j);
@@ -736,6 +764,40 @@ int32_t or_offspring(or_state* s, uint32_t g, int32_t j, float* geno, float* fit
   evaluate(s, geno, fit, desc);
   if (parents) { parents[0] = par[0]; parents[1] = par[1]; }
   return 0;
+}
+
+/* Offspring js[0 .. count) of generation g >= 1 from the archive as it
+ * stands now: objectives, descriptors (D per offspring) and parent pairs,
+ * computed in parallel.  Nothing is inserted. */
+int32_t or_offspring_many(or_state* s, uint32_t g, const int32_t* js, int32_t count,
+                          float* fit, float* desc, int32_t* parents) {
+  const int32_t D = s->cfg.D, n = s->n;
+  if (g == 0) return -1;
+  const int32_t nocc = build_occ_list(s);
+  if (nocc == 0) return -1;
+#pragma omp parallel
+  {
+    float* x = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
+    float d4[4];
+#pragma omp for schedule(dynamic, 1)
+    for (int32_t i = 0; i < count; ++i) {
+      make_offspring(s, g, js[i], nocc, x, parents + 2 * i);
+      evaluate(s, x, &fit[i], d4);
+      for (int32_t k = 0; k < D; ++k) desc[(size_t)i * D + k] = d4[k];
+    }
+    free(x);
+  }
+  return 0;
+}
+
+int32_t or_set_threads(int32_t n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+  return (int32_t)omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
 }
 
 /* Cell mapping and insertion driven by externally computed objectives and

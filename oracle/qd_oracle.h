@@ -39,6 +39,9 @@ typedef struct {
   int32_t cvt_iters;    /*      (0 = centroids stay the uniform draws)          */
   int32_t death_mode;   /* policies: 0 none, 1 truncate at failure, 2 discard   */
   float death_below;    /*   failure: new state component 0 below this          */
+  int32_t init_mode;    /* test functions' first batch: 0 every gene U[lo, hi);  */
+                        /*   1 as 0 plus one level per genotype half, uniform   */
+                        /*   over that descriptor dimension's box               */
   uint64_t seed;
 } or_config;
 
@@ -72,6 +75,10 @@ void     or_philox_many(const uint32_t* ctr, const uint32_t key[2], uint32_t* ou
                         int64_t count);
 void     or_normal_many(const uint32_t* x, float* out, int64_t count);
 
+/* Threads of the per-offspring loops (OpenMP; insertion always runs in one
+ * thread).  n <= 0 leaves the current setting; returns the number in use. */
+int32_t   or_set_threads(int32_t n);
+
 /* ---- the run ---- */
 int32_t   or_genotype_len(const or_config* cfg);
 int32_t   or_env_len(const or_config* cfg);
@@ -82,6 +89,8 @@ int32_t   or_init(or_state* s);                    /* setup + generation 0      
 int32_t   or_generation(or_state* s, uint32_t g);  /* one generation, g >= 1      */
 int32_t   or_offspring(or_state* s, uint32_t g, int32_t j, float* geno, float* fit,
                        float* desc, int32_t* parents);
+int32_t   or_offspring_many(or_state* s, uint32_t g, const int32_t* js, int32_t count,
+                            float* fit, float* desc, int32_t* parents);
 int32_t   or_insert_driven(or_state* s, const float* fit, const float* desc,
                            const float* geno, int32_t nb, int32_t* cell, uint8_t* won);
 void      or_stats(const or_state* s, double offset, double out[3]);

@@ -21,7 +21,7 @@ namespace qd {
 // (item, individual, generation, stream tag); key = the 64-bit seed.
 // ---------------------------------------------------------------------------
 enum : uint32_t { kTagInit = 0, kTagSelect = 1, kTagIso = 2, kTagCentroid = 3, kTagEnv = 4,
-                  kTagCvtSample = 5 };
+                  kTagCvtSample = 5, kTagInitLevel = 6 };
 
 struct Key {
   uint32_t k0, k1;

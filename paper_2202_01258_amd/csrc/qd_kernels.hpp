@@ -39,6 +39,7 @@ struct Params {
   int grid[4];
   float lo[4], hi[4], span[4];    // span = hi - lo in fp32
   float iso_sigma, line_sigma, init_lo, init_span;
+  int init_mode;                  // first batch: 0 uniform genes, 1 plus a level per half
   int obs, hid, act, T;
   Key key;
   int bucket_res, num_buckets;
@@ -131,10 +132,23 @@ __device__ __forceinline__ float4 make_genes(const Params& p, const Pair& q, uin
                                              int base) {
   if (GEN0) {
     const uint4 x = philox((uint32_t)(base >> 2), (uint32_t)j, 0u, kTagInit, p.key);
-    return make_float4(fma32(unit24(x.x), p.init_span, p.init_lo),
-                       fma32(unit24(x.y), p.init_span, p.init_lo),
-                       fma32(unit24(x.z), p.init_span, p.init_lo),
-                       fma32(unit24(x.w), p.init_span, p.init_lo));
+    float4 v = make_float4(fma32(unit24(x.x), p.init_span, p.init_lo),
+                           fma32(unit24(x.y), p.init_span, p.init_lo),
+                           fma32(unit24(x.z), p.init_span, p.init_lo),
+                           fma32(unit24(x.w), p.init_span, p.init_lo));
+    if (p.init_mode == 1) {
+      // spread first batch: a level per genotype half, uniform over that
+      // descriptor dimension's box (word h of block (0, j, 0, INIT_LEVEL))
+      const uint4 y = philox(0u, (uint32_t)j, 0u, kTagInitLevel, p.key);
+      const float l0 = fma32(unit24(y.x), p.span[0], p.lo[0]);
+      const float l1 = fma32(unit24(y.y), p.span[1], p.lo[1]);
+      const int half = p.n >> 1;
+      v.x = (base < half ? l0 : l1) + v.x;
+      v.y = (base + 1 < half ? l0 : l1) + v.y;
+      v.z = (base + 2 < half ? l0 : l1) + v.z;
+      v.w = (base + 3 < half ? l0 : l1) + v.w;
+    }
+    return v;
   } else {
     // wave-uniform row pointer + 32-bit unsigned byte offset (rows are far
     // below 4 GiB): the address form of a scalar base and a vector offset
@@ -361,7 +375,10 @@ __device__ __forceinline__ int cvt_cell_rows(const Params& p, float d0, float d1
   min_pair_row<4>(best, best_idx);
   min_pair_row<2>(best, best_idx);
   min_pair_row<1>(best, best_idx);
-  const int res = nan ? -1 : (inside && cnt <= QD_CAND_SLOTS ? best_idx : -2);
+  // an empty list (never built: every bucket lists the centroid that sets its
+  // distance bound) would leave best_idx unset; the ring search takes it then
+  const int res = nan ? -1
+                      : (inside && cnt <= QD_CAND_SLOTS && best_idx != 0x7fffffff ? best_idx : -2);
   return __shfl(res, (lane & 3) * 16, 64);
 }
 

@@ -65,6 +65,8 @@ qd_status validate(const qd_config* c) {
   if (c->death_mode < 0 || c->death_mode > 2 || (c->death_mode != 0 && !is_mlp(c)) ||
       c->death_below != c->death_below)
     return QD_ERR_INVALID_ARG;
+  if (c->init_mode < 0 || c->init_mode > 1 || (c->init_mode != 0 && is_mlp(c)))
+    return QD_ERR_INVALID_ARG;
   const int D = c->desc_dim;
   if (is_mlp(c)) {
     if (c->genotype_dim != 0 || D != 4) return QD_ERR_INVALID_ARG;
@@ -350,6 +352,7 @@ qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
   p.iso_sigma = c->iso_sigma;
   p.line_sigma = c->line_sigma;
   p.init_lo = c->init_lo;
+  p.init_mode = c->init_mode;
   {
     const volatile float hi = c->init_hi, lo = c->init_lo;
     p.init_span = hi - lo;

@@ -15,7 +15,7 @@ from . import workloads as W
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqd.so")
 
-ABI_VERSION = 5
+ABI_VERSION = 6
 CAND_SLOTS = 16
 NORMAL_ROWS = 385
 QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
@@ -49,7 +49,8 @@ class QdConfig(C.Structure):
         ("mlp_obs", C.c_int32), ("mlp_hidden", C.c_int32), ("mlp_act", C.c_int32),
         ("episode_len", C.c_int32), ("keep_offspring", C.c_int32),
         ("cvt_samples", C.c_int32), ("cvt_iters", C.c_int32),
-        ("death_mode", C.c_int32), ("death_below", C.c_float), ("seed", C.c_uint64),
+        ("death_mode", C.c_int32), ("death_below", C.c_float), ("init_mode", C.c_int32),
+        ("seed", C.c_uint64),
     ]
 
 
@@ -133,6 +134,7 @@ def make_config(w: dict, keep_offspring: bool = False) -> QdConfig:
     c.keep_offspring = 1 if keep_offspring else 0
     c.cvt_samples, c.cvt_iters = w.get("cvt_samples", 0), w.get("cvt_iters", 0)
     c.death_mode, c.death_below = w.get("death_mode", 0), w.get("death_below", 0.0)
+    c.init_mode = w.get("init_mode", 0)
     c.seed = w["seed"]
     return c
 

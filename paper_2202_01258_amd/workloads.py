@@ -23,7 +23,7 @@ _BASE = dict(
     task=RASTRIGIN, tess=GRID, n=100, batch=128, D=2, grid=(100, 100), C=10000,
     lo=(-5.12, -5.12), hi=(5.12, 5.12), iso_sigma=0.005, line_sigma=0.05,
     init_lo=-0.1, init_hi=0.1, obs=27, hid=64, act=8, T=250, seed=0, generations=100,
-    cvt_samples=0, cvt_iters=0, death_mode=0, death_below=0.0,
+    cvt_samples=0, cvt_iters=0, death_mode=0, death_below=0.0, init_mode=0,
 )
 
 WORKLOADS = {
@@ -36,6 +36,12 @@ WORKLOADS = {
     "rastrigin_proj_cvt_b65536": dict(
         _BASE, task=RASTRIGIN_PROJ, tess=CVT, n=1000, batch=65536, grid=(0, 0),
         C=10000, generations=200),
+    # The same shape with a spread first batch: each individual adds one
+    # level per genotype half, uniform over the descriptor box, so the first
+    # batch fills nearly all 10^4 cells and parents are distinct rows.
+    "rastrigin_proj_cvt_b65536_spread": dict(
+        _BASE, task=RASTRIGIN_PROJ, tess=CVT, n=1000, batch=65536, grid=(0, 0),
+        C=10000, generations=200, init_mode=1),
     # Policy 27->64->64->8, T=250, CVT 1024 in [0,1]^4, N_B=8192, 100 generations.
     "mlp64_cvt_b8192": dict(
         _BASE, task=MLP_SYNTH, tess=CVT, n=0, batch=8192, D=4, grid=(0, 0, 0, 0), C=1024,

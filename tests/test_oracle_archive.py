@@ -161,6 +161,33 @@ def test_first_batch_is_uniform_init():
     assert abs(x.std() - 0.2 / np.sqrt(12)) < 2e-3
 
 
+def test_spread_first_batch():
+    """init_mode 1: individual j adds one level per genotype half, uniform over
+    that descriptor dimension's box, to the usual U[lo, hi) genes; the
+    projection descriptors of the first batch then cover the box, so a
+    65536-sized batch fills almost every one of 10^4 centroids' cells."""
+    w = workload("rastrigin_proj_cvt_b65536", batch=4096, n=40, init_mode=1, C=400)
+    o = O.Oracle(w)
+    o.init()
+    x = o.last_offspring().astype(np.float64)
+    h = x.shape[1] // 2
+    lev0 = x[:, :h].mean(1)
+    lev1 = x[:, h:].mean(1)
+    for lev, part in ((lev0, x[:, :h]), (lev1, x[:, h:])):
+        # every gene of a half within [level - 0.1, level + 0.1): the half's
+        # spread is that of the usual first batch
+        width = part.max(1) - part.min(1)
+        assert width.max() < 0.2 + 1e-5
+        u = (lev + 5.12) / 10.24
+        assert stats.kstest(np.clip(u, 0, 1), "uniform").pvalue > 1e-3
+    assert abs(np.corrcoef(lev0, lev1)[0, 1]) < 0.1
+    filled = int(o.archive()["occ"].sum())
+    assert filled >= 390                    # 4096 draws over 400 cells
+    plain = O.Oracle(workload("rastrigin_proj_cvt_b65536", batch=4096, n=40, C=400))
+    plain.init()
+    assert int(plain.archive()["occ"].sum()) < 10
+
+
 def test_selection_only_filled_cells_and_uniform():
     o = O.Oracle(workload("sphere_grid_b16384", batch=4096, n=8))
     o.init()

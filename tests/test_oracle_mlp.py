@@ -3,7 +3,20 @@
 * Zero weights from a zero state: a = 0, s = 0 forever, return 0 and
   descriptor sigmoid(0) = 1/2 exactly.
 * Against an fp64 numpy rollout built from matrix products and np.tanh
-  (a transposed weight block, a wrong bias slice or reward sign fails it).
+  (a transposed weight block, a wrong bias slice or reward sign fails it),
+  at the tolerance the method states (1e-5 relative on the return, 1e-5 of
+  the [0, 1] box on the descriptor) -- short random policies, and the two
+  policy configurations themselves (27-64-64-8 for T = 250, 27-128-128-8 for
+  T = 1000) with their own Glorot first batch and environment, also with the
+  weights scaled by 1.5 so that returns reach hundreds.
+* Against a second fp32 rollout written with the plainest summation order
+  (every dot product one chain in ascending input order) and numpy's fp32
+  tanh/exp: the oracle's interleaved orders (four partial sums in the hidden
+  layers, eight slices in the output layer) are one rounding of the same
+  sums and stay within the same tolerance of both.
+* On random policies at the configurations' sizes, whose returns can cancel,
+  the return error is bounded by 1e-5 times the sum of the rewards' absolute
+  values (the condition of a sum).
 * Glorot-uniform first batch within its limits, zero biases; environment
   entries 0.1 N(0,1).
 """
@@ -26,16 +39,129 @@ def split(w, obs, hid, act):
     return out
 
 
-def rollout64(w, obs, hid, act, T, A, B, s0):
+def rollout64(w, obs, hid, act, T, A, B, s0, abs_sum=False):
     W1, b1, W2, b2, W3, b3 = [x.astype(np.float64) for x in split(w, obs, hid, act)]
     A, B, s = A.astype(np.float64), B.astype(np.float64), s0.astype(np.float64)
-    ret, dsum = 0.0, np.zeros(4)
+    ret, dsum, absr = 0.0, np.zeros(4), 0.0
     for _ in range(T):
         a = np.tanh(W3 @ np.tanh(W2 @ np.tanh(W1 @ s + b1) + b2) + b3)
         s = np.tanh(A @ s + B @ a)
-        ret += s[0] - 0.5 * a @ a
+        r = s[0] - 0.5 * a @ a
+        ret += r
+        absr += abs(r)
         dsum += 1.0 / (1.0 + np.exp(-s[1:5]))
+    if abs_sum:
+        return ret, dsum / T, absr
     return ret, dsum / T
+
+
+def fma32(a, b, c):
+    """fp32 a*b + c rounded once from its exact value in fp64 (the product of
+    two fp32 numbers is exact there; the sum is then rounded to fp64 first,
+    so rare ties may round differently from a true fma)."""
+    return (np.asarray(a, np.float64) * np.asarray(b, np.float64)
+            + np.asarray(c, np.float64)).astype(np.float32)
+
+
+def rollout32_plain(w, obs, hid, act, T, A, B, s0):
+    """A second fp32 rollout: every dot product (layers, A s + B a, |a|^2) is
+    one fma chain in ascending input order, vectorised over outputs; tanh and
+    exp are numpy's fp32 functions."""
+    W1, b1, W2, b2, W3, b3 = split(w, obs, hid, act)
+
+    def dense(W, b, x):
+        acc = np.zeros(W.shape[0], np.float32)
+        for k in range(W.shape[1]):
+            acc = fma32(W[:, k], x[k], acc)
+        return np.tanh(acc + b)
+
+    s = s0.astype(np.float32)
+    ret, dsum = np.float32(0.0), np.zeros(4, np.float32)
+    one = np.float32(1.0)
+    for _ in range(T):
+        a = dense(W3, b3, dense(W2, b2, dense(W1, b1, s)))
+        acc = np.zeros(obs, np.float32)
+        for k in range(obs):
+            acc = fma32(A[:, k], s[k], acc)
+        for k in range(act):
+            acc = fma32(B[:, k], a[k], acc)
+        s = np.tanh(acc)
+        q = np.float32(0.0)
+        for o in range(act):
+            q = fma32(a[o], a[o], q)
+        ret = np.float32(ret + fma32(np.float32(-0.5), q, s[0]))
+        dsum = (dsum + one / (one + np.exp(-s[1:5]))).astype(np.float32)
+    return ret, dsum / np.float32(T)
+
+
+def config_policies(name, count, scale):
+    """The first `count` first-batch policies of a policy configuration (the
+    oracle's Glorot draws), weights times `scale`, with its environment."""
+    w = workload(name, batch=count)
+    o = O.Oracle(w)
+    o.init()
+    obs, act = w["obs"], w["act"]
+    env = o.env()
+    A = env[: obs * obs].reshape(obs, obs)
+    B = env[obs * obs: obs * obs + obs * act].reshape(obs, act)
+    s0 = env[obs * obs + obs * act:]
+    x = (o.last_offspring() * np.float32(scale)).astype(np.float32)
+    return w, x, A, B, s0
+
+
+@pytest.mark.parametrize("name", ["mlp64_cvt_b8192", "mlp128_cvt_b65536"])
+@pytest.mark.parametrize("scale", [1.0, 1.5])
+def test_configuration_rollouts_match_fp64(name, scale):
+    """27-64-64-8 over T = 250 and 27-128-128-8 over T = 1000 (the policy
+    configurations), 16 individuals each: the oracle's fp32 rollout is within
+    1e-5 relative of fp64 on the return and 1e-5 on the descriptor."""
+    w, x, A, B, s0 = config_policies(name, 16, scale)
+    obs, hid, act, T = w["obs"], w["hid"], w["act"], w["T"]
+    returns = []
+    for j in range(x.shape[0]):
+        f, d = O.mlp_rollout(x[j], obs, hid, act, T, A, B, s0)
+        rf, rd = rollout64(x[j], obs, hid, act, T, A, B, s0)
+        assert abs(f - rf) <= 1e-5 * max(abs(rf), 1e-6), (j, f, rf)
+        assert np.max(np.abs(d - rd)) <= 1e-5, (j, d, rd)
+        returns.append(abs(rf))
+    if scale > 1.0:
+        assert max(returns) > 100.0          # returns far from 0 are among them
+
+
+@pytest.mark.parametrize("name", ["mlp64_cvt_b8192", "mlp128_cvt_b65536"])
+@pytest.mark.parametrize("scale", [1.0, 1.5])
+def test_configuration_rollouts_match_the_plain_order(name, scale):
+    """The oracle against the plain-order fp32 rollout, and that one against
+    fp64: both fp32 orders lie within the same 1e-5 tolerance."""
+    w, x, A, B, s0 = config_policies(name, 2, scale)
+    obs, hid, act, T = w["obs"], w["hid"], w["act"], w["T"]
+    for j in range(x.shape[0]):
+        f, d = O.mlp_rollout(x[j], obs, hid, act, T, A, B, s0)
+        pf, pd = rollout32_plain(x[j], obs, hid, act, T, A, B, s0)
+        rf, rd = rollout64(x[j], obs, hid, act, T, A, B, s0)
+        assert abs(f - pf) <= 1e-5 * max(abs(pf), 1e-6), (j, f, pf)
+        assert np.max(np.abs(d - pd)) <= 1e-5
+        assert abs(pf - rf) <= 1e-5 * max(abs(rf), 1e-6), (j, pf, rf)
+        assert np.max(np.abs(pd - rd)) <= 1e-5
+
+
+@pytest.mark.parametrize("hid,T", [(64, 250), (128, 1000)])
+def test_random_policies_at_configuration_sizes(hid, T):
+    """Random (non-Glorot) policies whose returns can cancel: the return
+    error is within 1e-5 of the sum of the rewards' magnitudes, the
+    descriptor within 1e-5."""
+    obs, act = 27, 8
+    n = hid * obs + hid + hid * hid + hid + act * hid + act
+    rng = np.random.default_rng(hid + T)
+    for trial in range(3):
+        w = rng.normal(0, 0.6 / np.sqrt(hid), n).astype(np.float32)
+        A = rng.normal(0, 0.3, (obs, obs)).astype(np.float32)
+        B = rng.normal(0, 0.5, (obs, act)).astype(np.float32)
+        s0 = rng.normal(0, 0.5, obs).astype(np.float32)
+        f, d = O.mlp_rollout(w, obs, hid, act, T, A, B, s0)
+        rf, rd, absr = rollout64(w, obs, hid, act, T, A, B, s0, abs_sum=True)
+        assert abs(f - rf) <= 1e-5 * absr, (trial, f, rf, absr)
+        assert np.max(np.abs(d - rd)) <= 1e-5
 
 
 def test_zero_policy_zero_state():
@@ -61,7 +187,7 @@ def test_rollout_matches_fp64(hid, T):
         s0 = rng.normal(0, 0.5, obs).astype(np.float32)
         f, d = O.mlp_rollout(w, obs, hid, act, T, A, B, s0)
         rf, rd = rollout64(w, obs, hid, act, T, A, B, s0)
-        assert abs(f - rf) <= 1e-4 * max(1.0, abs(rf)), (f, rf)
+        assert abs(f - rf) <= 1e-5 * max(abs(rf), 1e-6), (f, rf)
         np.testing.assert_allclose(d, rd, atol=2e-6)
 
 
@@ -155,7 +281,7 @@ def test_death_truncates_like_fp64(mode):
         if mode == 2:
             assert np.isnan(f)
         else:
-            assert abs(f - fit) <= 1e-4 * max(1.0, abs(fit)), (f, fit)
+            assert abs(f - fit) <= 1e-5 * max(abs(fit), 1e-6), (f, fit)
         np.testing.assert_allclose(d, desc, atol=2e-6)
         checked += 1
     assert checked >= 6

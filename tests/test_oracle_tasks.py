@@ -83,6 +83,42 @@ def test_projection_descriptor():
     assert np.max(np.abs(d - ref)) < 1e-5
 
 
+@pytest.mark.parametrize("dist", ["init", "box", "beyond"])
+def test_projection_and_objective_at_n1000_match_plain_and_fp64(dist):
+    """The two-half projection descriptor and the objective at n = 1000, in
+    the R64 order, against the plainest fp32 order (one running sum in gene
+    order) and against fp64: within 1e-5 of the box (hi - lo = 10.24) for
+    the descriptor and 1e-5 relative for the objective, for genes from the
+    configuration's first batch, over the whole box, and partly beyond it
+    (clipped)."""
+    n, lo, hi = 1000, np.float32(-5.12), np.float32(5.12)
+    rng = np.random.default_rng({"init": 1, "box": 2, "beyond": 3}[dist])
+    span = float(hi - lo)
+    for _ in range(50):
+        if dist == "init":
+            x = rng.uniform(-0.1, 0.1, n)
+        elif dist == "box":
+            x = rng.uniform(-5.12, 5.12, n) * rng.uniform(0, 1) + rng.uniform(-4, 4)
+        else:
+            x = rng.normal(rng.uniform(-6, 6), 3.0, n)
+        x = x.astype(np.float32)
+        f, d = O.eval_testfn(RASTRIGIN_PROJ, x)
+        cl = np.clip(x, lo, hi)
+        # plain fp32: a running sum in gene order, then the IEEE quotient
+        plain = [np.add.accumulate(cl[:500], dtype=np.float32)[-1] / np.float32(500),
+                 np.add.accumulate(cl[500:], dtype=np.float32)[-1] / np.float32(500)]
+        ref = [cl[:500].astype(np.float64).mean(), cl[500:].astype(np.float64).mean()]
+        assert np.max(np.abs(d - np.float32(plain))) <= 1e-5 * span
+        assert np.max(np.abs(d - np.array(ref))) <= 1e-5 * span
+        assert np.max(np.abs(np.float32(plain) - np.array(ref))) <= 1e-5 * span
+        x64 = x.astype(np.float64)
+        terms32 = (x * x + np.float32(20.0) * np.sin(np.pi * x64).astype(np.float32) ** 2)
+        plain_f = -np.add.accumulate(terms32.astype(np.float32), dtype=np.float32)[-1]
+        ref_f = rastrigin64(x)
+        assert abs(f - ref_f) <= 1e-5 * abs(ref_f)
+        assert abs(plain_f - ref_f) <= 1e-5 * abs(ref_f)
+
+
 def test_grid_edges_and_layout():
     lo, hi, grid = [-5.12, -5.12], [5.12, 5.12], [100, 100]
     assert O.grid_cell([-5.12, -5.12], grid, lo, hi) == 0
