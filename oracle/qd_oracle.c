@@ -766,22 +766,27 @@ int32_t or_offspring(or_state* s, uint32_t g, int32_t j, float* geno, float* fit
   return 0;
 }
 
-/* Offspring js[0 .. count) of generation g >= 1 from the archive as it
- * stands now: objectives, descriptors (D per offspring) and parent pairs,
- * computed in parallel.  Nothing is inserted. */
+/* Offspring js[0 .. count) of generation g from the archive as it stands now
+ * (g == 0: members of the random first batch): objectives, descriptors (D per
+ * offspring) and parent pairs (-1 for the first batch), computed in parallel.
+ * Nothing is inserted. */
 int32_t or_offspring_many(or_state* s, uint32_t g, const int32_t* js, int32_t count,
                           float* fit, float* desc, int32_t* parents) {
   const int32_t D = s->cfg.D, n = s->n;
-  if (g == 0) return -1;
-  const int32_t nocc = build_occ_list(s);
-  if (nocc == 0) return -1;
+  const int32_t nocc = g == 0 ? 0 : build_occ_list(s);
+  if (g != 0 && nocc == 0) return -1;
 #pragma omp parallel
   {
     float* x = (float*)malloc(sizeof(float) * (size_t)(n > 0 ? n : 1));
     float d4[4];
 #pragma omp for schedule(dynamic, 1)
     for (int32_t i = 0; i < count; ++i) {
-      make_offspring(s, g, js[i], nocc, x, parents + 2 * i);
+      if (g == 0) {
+        init_genotype(s, js[i], x);
+        parents[2 * i] = parents[2 * i + 1] = -1;
+      } else {
+        make_offspring(s, g, js[i], nocc, x, parents + 2 * i);
+      }
       evaluate(s, x, &fit[i], d4);
       for (int32_t k = 0; k < D; ++k) desc[(size_t)i * D + k] = d4[k];
     }

@@ -1,7 +1,9 @@
 """Summarise rocprofv3 results databases (SQLite) as text tables.
 
-  python -m paper_2202_01258_amd.rocprof_summary <results.db> [--top N]
-      kernel trace: kernel, calls, total and average duration
+  python -m paper_2202_01258_amd.rocprof_summary <results.db> [--top N] [--per-archive]
+      kernel trace: kernel, calls, total and average duration; with
+      --per-archive one table per archive the program created (dispatches in
+      start order, a new archive beginning at each k_clear_archive)
   python -m paper_2202_01258_amd.rocprof_summary --pmc <results.db> [--top N]
       counters (--pmc runs): kernel, counter, dispatches, mean value per dispatch
   python -m paper_2202_01258_amd.rocprof_summary --traffic KERNEL \
@@ -104,17 +106,46 @@ def recorded_valu(summary_path: str, kernel: str) -> float | None:
     return _recorded(summary_path, VALU_TAG, kernel)
 
 
-def summary(db_path: str, top: int = 20) -> str:
-    con = _open(db_path)
-    rows = con.execute(
-        "select name, count(*), sum(end - start), avg(end - start), min(end - start), "
-        "max(end - start) from kernels group by name order by sum(end - start) desc").fetchall()
-    total = sum(r[2] for r in rows) or 1
+def _table(rows, top: int) -> list[str]:
+    """rows: (name, duration_ns) in any order -> per-kernel statistics lines."""
+    per: dict[str, list[int]] = {}
+    for name, dur in rows:
+        per.setdefault(name, []).append(dur)
+    stats = sorted(((n, len(d), sum(d), min(d), max(d)) for n, d in per.items()),
+                   key=lambda r: -r[2])
+    total = sum(r[2] for r in stats) or 1
     out = [f"{'kernel':70s} {'calls':>6s} {'total_us':>11s} {'avg_us':>9s} "
            f"{'min_us':>9s} {'max_us':>9s} {'pct':>6s}"]
-    for name, calls, tot, avg, mn, mx in rows[:top]:
-        out.append(f"{name[:70]:70s} {calls:6d} {tot / 1e3:11.3f} {avg / 1e3:9.3f} "
+    for name, calls, tot, mn, mx in stats[:top]:
+        out.append(f"{name[:70]:70s} {calls:6d} {tot / 1e3:11.3f} {tot / calls / 1e3:9.3f} "
                    f"{mn / 1e3:9.3f} {mx / 1e3:9.3f} {100.0 * tot / total:6.2f}")
+    return out
+
+
+def split_per_archive(rows):
+    """Dispatches (name, start, end) in start order, cut into one run per
+    archive: each archive's set-up begins with k_clear_archive; what comes
+    before the first one forms a run of its own."""
+    runs, cur = [], []
+    for name, start, end in sorted(rows, key=lambda r: r[1]):
+        if "k_clear_archive" in name and cur:
+            runs.append(cur)
+            cur = []
+        cur.append((name, end - start))
+    if cur:
+        runs.append(cur)
+    return runs
+
+
+def summary(db_path: str, top: int = 20, per_archive: bool = False) -> str:
+    con = _open(db_path)
+    rows = con.execute("select name, start, end from kernels").fetchall()
+    if not per_archive:
+        return "\n".join(_table([(n, e - s) for n, s, e in rows], top))
+    out = []
+    for k, run in enumerate(split_per_archive(rows)):
+        out.append(f"-- archive {k} (dispatches {len(run)})")
+        out.extend(_table(run, top))
     return "\n".join(out)
 
 
@@ -184,6 +215,7 @@ def main():
     ap.add_argument("--traffic", metavar="KERNEL")
     ap.add_argument("--valu", metavar="KERNEL")
     ap.add_argument("--copy-mib", type=int, default=256)
+    ap.add_argument("--per-archive", action="store_true")
     a = ap.parse_args()
     if a.traffic:
         if len(a.db) != 4:
@@ -192,7 +224,7 @@ def main():
     elif a.valu:
         print(valu(a.valu, a.db[0]))
     else:
-        print(pmc_summary(a.db[0], a.top) if a.pmc else summary(a.db[0], a.top))
+        print(pmc_summary(a.db[0], a.top) if a.pmc else summary(a.db[0], a.top, a.per_archive))
 
 
 if __name__ == "__main__":

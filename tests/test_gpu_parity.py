@@ -195,6 +195,8 @@ def test_generations_driven_bit_exact(name):
     ("sphere_grid_b16384", {}, 500),                         # the full configuration
     ("rastrigin_proj_cvt_b65536", dict(batch=2048), 12),
     ("rastrigin_proj_cvt_b65536", {}, 3),                    # the benchmark configuration
+    # its shape with a spread first batch: ~10^4 filled cells, distinct parents
+    ("rastrigin_proj_cvt_b65536_spread", {}, 3),
     # first batch over the whole box: thousands of new cells and winners in
     # every early generation (regeneration and compaction at full load)
     ("rastrigin_grid_b128", dict(batch=4096, init_lo=-5.12, init_hi=5.12, seed=2), 40),
@@ -274,6 +276,10 @@ def check_driven_generation(a, o, w, g):
         np.testing.assert_array_equal(par, gb["parents"][j])
         assert gb["fit"][j] == fit
         np.testing.assert_array_equal(gb["desc"][j], desc)
+    # the winners' genotypes, made by the oracle from the archive before the
+    # insertion (afterwards new cells would change the selection)
+    winners = np.nonzero(gb["won"])[0][:8]
+    expect = {int(j): o.offspring(g, int(j))[0] for j in winners}
     cell, won = o.insert_driven(gb["fit"], gb["desc"])
     np.testing.assert_array_equal(gb["cell"], cell)
     np.testing.assert_array_equal(gb["won"], won)
@@ -284,21 +290,24 @@ def check_driven_generation(a, o, w, g):
     np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
     np.testing.assert_array_equal(post["desc"][filled], oa["desc"][filled])
     # winners' rows: regenerated on the GPU, recomputed here
-    for j in np.nonzero(won)[0][:8]:
-        geno, fit, desc, _ = o.offspring(g, int(j))
+    for j, geno in expect.items():
         np.testing.assert_array_equal(post["geno"][gb["cell"][j]], geno)
     # the tolerance the method states, for the record
     assert rel_err(post["fit"][filled], oa["fit"][filled], 1e-6) <= 1e-5
     return int(won.sum())
 
 
-@pytest.mark.parametrize("batch", [65536, 131072])
-def test_full_size_rastrigin_projection_sampled(batch):
+@pytest.mark.parametrize("name,batch", [("rastrigin_proj_cvt_b65536", 65536),
+                                        ("rastrigin_proj_cvt_b65536", 131072),
+                                        ("rastrigin_proj_cvt_b65536_spread", 65536)])
+def test_full_size_rastrigin_projection_sampled(name, batch):
     """n = 1000, CVT 10^4 at N_B = 65536 (the benchmark's launch configuration)
-    and at 131072 (the top of the batch-size sweep).  Every offspring's cell
-    and the whole insertion are checked (driven), and sampled offspring
-    genotypes/objectives/descriptors from the oracle."""
-    w = W.workload("rastrigin_proj_cvt_b65536", batch=batch)
+    and at 131072 (the top of the batch-size sweep), and the same shape with
+    a spread first batch (nearly every cell filled, thousands of winners per
+    generation).  Every offspring's cell and the whole insertion are checked
+    (driven), and sampled offspring genotypes/objectives/descriptors from the
+    oracle."""
+    w = W.workload(name, batch=batch)
     say(f"full size rastrigin projection N_B={batch}: init")
     a = qd().Archive(w)
     o = O.Oracle(w)
@@ -419,13 +428,15 @@ def test_mlp_full_size_sampled(name, batch, samples):
     np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
 
 
-@pytest.mark.parametrize("name,G", [("mlp64_cvt_b8192", 100), ("mlp128_cvt_b65536", 50)])
-def test_policy_configuration_at_last_generation_driven(name, G):
+@pytest.mark.parametrize("name,G,count", [("mlp64_cvt_b8192", 100, None),
+                                          ("mlp128_cvt_b65536", 50, 512)])
+def test_policy_configuration_at_last_generation_driven(name, G, count):
     """A policy configuration (27-64-64-8, T = 250, N_B = 8192; 27-128-128-8,
     T = 1000, N_B = 65536) run on the GPU alone for the paper's G - 1
     generations, then generation G checked from the archive the GPU reached:
-    sampled rollouts, every cell and the insertion, and the winners'
-    regenerated rows."""
+    rollouts against the oracle's (all 8192 of the first configuration, 512
+    of the second; the oracle runs them on every host thread), every cell
+    and the insertion, and the winners' regenerated rows."""
     w = W.workload(name)
     say(f"policy configuration {name}: init, {G - 1} free-running generations")
     a = qd().Archive(w)
@@ -439,12 +450,15 @@ def test_policy_configuration_at_last_generation_driven(name, G):
     gb = a.last_batch()
     o.set_archive(pre["geno"], pre["fit"], pre["desc"], pre["occ"])
     rng = np.random.default_rng(g)
-    for j in np.concatenate([[0, w["batch"] - 1], rng.integers(0, w["batch"], 4)]):
-        say(f"  oracle rollout j={j}")
-        geno, fit, desc, par = o.offspring(g, int(j))
-        np.testing.assert_array_equal(par, gb["parents"][j])
-        assert gb["fit"][j] == fit, (j, gb["fit"][j], fit)
-        np.testing.assert_array_equal(gb["desc"][j], desc)
+    js = (np.arange(w["batch"]) if count is None else
+          np.unique(np.concatenate([[0, w["batch"] - 1], rng.integers(0, w["batch"], count)])))
+    say(f"  oracle rollouts: {js.size} on {O.set_threads(0)} threads")
+    fit, desc, par = o.offspring_many(g, js)
+    np.testing.assert_array_equal(par, gb["parents"][js])
+    np.testing.assert_array_equal(gb["fit"][js].view(np.uint32), fit.view(np.uint32))
+    np.testing.assert_array_equal(gb["desc"][js], desc)
+    # winners' genotypes from the archive before the insertion
+    expect = {int(j): o.offspring(g, int(j))[0] for j in np.nonzero(gb["won"])[0][:4]}
     cell, won = o.insert_driven(gb["fit"], gb["desc"])
     np.testing.assert_array_equal(gb["cell"], cell)
     np.testing.assert_array_equal(gb["won"], won)
@@ -453,9 +467,33 @@ def test_policy_configuration_at_last_generation_driven(name, G):
     filled = oa["occ"] == 1
     np.testing.assert_array_equal(post["fit"][filled], oa["fit"][filled])
     np.testing.assert_array_equal(post["desc"][filled], oa["desc"][filled])
-    for j in np.nonzero(won)[0][:4]:
-        geno, _, _, _ = o.offspring(g, int(j))
+    for j, geno in expect.items():
         np.testing.assert_array_equal(post["geno"][gb["cell"][j]], geno)
+
+
+def test_policy_configuration_end_to_end():
+    """27-64-64-8, T = 250, N_B = 8192, CVT 1024 (the configuration in full
+    size) free-running for 4 generations on both sides: every rollout, the
+    archive and the QD-score (1e-4 relative asked; equal here)."""
+    G = 4
+    w = W.workload("mlp64_cvt_b8192")
+    say(f"policy configuration end to end, G={G}, oracle on {O.set_threads(0)} threads")
+    a = qd().Archive(w)
+    o = O.Oracle(w)
+    o.init()
+    for g in range(1, G + 1):
+        a.generation(g)
+        o.generation(g)
+        say(f"  generation {g}")
+        gb, ob = a.last_batch(), o.last_batch()
+        np.testing.assert_array_equal(gb["fit"].view(np.uint32), ob["fit"].view(np.uint32))
+        np.testing.assert_array_equal(gb["desc"], ob["desc"])
+        np.testing.assert_array_equal(gb["won"], ob["won"])
+    gs, os_ = a.stats(), o.stats()
+    assert gs["num_occupied"] == os_["coverage"]
+    assert abs(gs["qd_score"] - os_["qd_score"]) <= 1e-4 * abs(os_["qd_score"])
+    assert gs["qd_score"] == pytest.approx(os_["qd_score"], rel=1e-12)
+    assert_archive_equal(a.snapshot(), o.archive(), o.n, f"after {G} generations")
 
 
 @pytest.mark.parametrize("kw", [dict(batch=1), dict(n=2, batch=5), dict(n=101, batch=9),

@@ -58,3 +58,12 @@ def test_digest_ignores_comments_and_layout_but_not_code(tmp_path):
     assert R._code_text(str(a)) == R._code_text(str(b))
     assert R._code_text(str(a)) != R._code_text(str(c))
     assert b'"// kept"' in R._code_text(str(a))
+
+
+def test_split_per_archive():
+    rows = [("copy", 0, 5), ("k_clear_archive(a)", 10, 11), ("k_vary_eval<2>", 12, 20),
+            ("k_vary_eval<2>", 21, 25), ("k_clear_archive(a)", 30, 31), ("k_vary_eval<2>", 32, 42)]
+    runs = R.split_per_archive(list(reversed(rows)))
+    assert [len(r) for r in runs] == [1, 3, 2]
+    assert runs[1][1:] == [("k_vary_eval<2>", 8), ("k_vary_eval<2>", 4)]
+    assert runs[2] == [("k_clear_archive(a)", 1), ("k_vary_eval<2>", 10)]
