@@ -208,6 +208,21 @@ qd_status qd_generations(qd_archive* h, uint32_t first_gen, uint32_t count, void
  * copied into *out.  Synchronises `stream` (the only call that does). */
 qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_stats* out);
 
+/* For callers that cannot allocate device memory or use workspace memory at
+ * this point (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same statistics as qd_archive_stats(), staged
+ * on the device in the library's own scratch (a file-scope device array of
+ * 256 bytes, one per GPU, held until the process ends) instead of the
+ * workspace's statistics buffer.  Allocates nothing (no hipMalloc, hipFree or
+ * allocating library call).  The scratch holds four results whatever the
+ * archive's size, so no archive is too large for it.  The handle's device
+ * (the one current at qd_archive_init) must be current: QD_ERR_INVALID_ARG
+ * otherwise, and for a null handle or out.  Synchronises `stream`.  Every
+ * call on one GPU shares that GPU's scratch, which keeps the last call's
+ * results: calls that overlap on one GPU (several host threads, or streams
+ * not ordered with one another) race. */
+qd_status qd_archive_stats_noalloc(qd_archive* h, double qd_offset, void* stream, qd_stats* out);
+
 /* The layout the handle was created with. */
 qd_status qd_archive_layout(const qd_archive* h, qd_layout* out);
 

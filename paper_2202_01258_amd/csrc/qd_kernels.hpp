@@ -935,9 +935,11 @@ __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
 }
 
 // ---------------------------------------------------------------------------
-// Statistics over the archive (fp64 accumulation).  One workgroup.
+// Statistics over the archive (fp64 accumulation).  One workgroup; the four
+// results go to out[0 .. 3] (the workspace's statistics buffer, or the
+// library's own device scratch for callers that cannot allocate).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void k_stats(const Params p, double offset) {
+__global__ __launch_bounds__(1024) void k_stats(const Params p, double offset, double* out) {
   __shared__ double s_sum[16];
   __shared__ double s_best[16];
   __shared__ int s_cnt[16];
@@ -972,10 +974,10 @@ __global__ __launch_bounds__(1024) void k_stats(const Params p, double offset) {
       tb = s_best[w] > tb ? s_best[w] : tb;
       tc += s_cnt[w];
     }
-    p.stats[0] = ts;
-    p.stats[1] = (double)tc;
-    p.stats[2] = tc ? tb : __builtin_nan("");
-    p.stats[3] = (double)p.counters[1];
+    out[0] = ts;
+    out[1] = (double)tc;
+    out[2] = tc ? tb : __builtin_nan("");
+    out[3] = (double)p.counters[1];
   }
 }
 

@@ -8,6 +8,7 @@
 #include <array>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -210,7 +211,17 @@ const NormalTable& normal_table() {
 
 }  // namespace
 
+// Device scratch of qd_archive_stats_noalloc: the statistics kernel's four
+// results, staged here instead of in the workspace, for callers that cannot
+// allocate.  Every GPU the library runs on holds its own copy until the
+// process ends; host code must use the per-device address from
+// hipGetSymbolAddress (the array's name is only a host-side stand-in).
+constexpr int kScratchDoubles = 32;   // 256 bytes
+static __device__ __align__(256) double scratch[kScratchDoubles];
+
+
 struct qd_archive {
+  int device = -1;          // the device current at qd_archive_init
   qd_config cfg;
   qd_layout lay;
   qd::Params p;
@@ -229,6 +240,26 @@ qd_status hip_fail(hipError_t e) {
   g_last_hip = e;
   return QD_ERR_HIP;
 }
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of `scratch` on device `dev` (which must be current), looked up
+// once per device.
+qd_status noalloc_scratch(int dev, double** out) {
+  if (dev < 0 || dev >= kMaxDevices) return QD_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol);
+    g_scratch_ptr[dev] = (double*)ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return QD_OK;
+}
+
 
 hipEvent_t take_event(qd_archive* h) {
   if (!h->pool.empty()) {
@@ -332,6 +363,25 @@ qd_status enqueue_generation(qd_archive* h, hipStream_t s, uint32_t g) {
   return e == hipSuccess ? QD_OK : hip_fail(e);
 }
 
+// k_stats into `dev` (4 doubles of device memory), then to *out; synchronises.
+qd_status stats_into(qd_archive* h, double qd_offset, hipStream_t s, double* dev, qd_stats* out) {
+  hipLaunchKernelGGL(qd::k_stats, dim3(1), dim3(1024), 0, s, h->p, qd_offset, dev);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e);
+  double host[4];
+  e = hipMemcpyAsync(host, dev, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e);
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e);
+  out->qd_score = host[0];
+  out->num_occupied = (int32_t)host[1];
+  out->coverage = host[1] / (double)h->cfg.num_cells;
+  out->best_fitness = (float)host[2];
+  out->flags = (uint32_t)host[3];
+  out->reserved = 0;
+  return QD_OK;
+}
+
 qd::Params make_params(const qd_config* c, const qd_layout* L, uint8_t* ws) {
   qd::Params p;
   std::memset(&p, 0, sizeof(p));
@@ -422,8 +472,18 @@ qd_status qd_archive_init(const qd_config* cfg, void* d_workspace, uint64_t work
   if (st != QD_OK) return st;
   if (((uintptr_t)d_workspace % kAlign) != 0) return QD_ERR_INVALID_ARG;
   if (workspace_bytes < L.workspace_bytes) return QD_ERR_WORKSPACE_TOO_SMALL;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return QD_ERR_HIP;
   qd_archive* h = new (std::nothrow) qd_archive();
   if (!h) return QD_ERR_INVALID_ARG;
+  h->device = dev;
+  {
+    // the no-allocation scratch's address on this device, looked up here once
+    // (a failure is reported by qd_archive_stats_noalloc, which retries)
+    double* scr = nullptr;
+    (void)noalloc_scratch(dev, &scr);
+    (void)hipGetLastError();
+  }
   h->cfg = *cfg;
   h->lay = L;
   h->p = make_params(cfg, &L, (uint8_t*)d_workspace);
@@ -494,22 +554,20 @@ qd_status qd_generations(qd_archive* h, uint32_t first_gen, uint32_t count, void
 
 qd_status qd_archive_stats(qd_archive* h, double qd_offset, void* stream, qd_stats* out) {
   if (!h || !out) return QD_ERR_INVALID_ARG;
-  hipStream_t s = (hipStream_t)stream;
-  hipLaunchKernelGGL(qd::k_stats, dim3(1), dim3(1024), 0, s, h->p, qd_offset);
-  hipError_t e = hipGetLastError();
+  return stats_into(h, qd_offset, (hipStream_t)stream, h->p.stats, out);
+}
+
+qd_status qd_archive_stats_noalloc(qd_archive* h, double qd_offset, void* stream, qd_stats* out) {
+  if (!h || !out) return QD_ERR_INVALID_ARG;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e);
-  double host[4];
-  e = hipMemcpyAsync(host, h->p.stats, sizeof(host), hipMemcpyDeviceToHost, s);
-  if (e != hipSuccess) return hip_fail(e);
-  e = hipStreamSynchronize(s);
-  if (e != hipSuccess) return hip_fail(e);
-  out->qd_score = host[0];
-  out->num_occupied = (int32_t)host[1];
-  out->coverage = host[1] / (double)h->cfg.num_cells;
-  out->best_fitness = (float)host[2];
-  out->flags = (uint32_t)host[3];
-  out->reserved = 0;
-  return QD_OK;
+  if (dev != h->device) return QD_ERR_INVALID_ARG;   // the handle's device must be current
+  double* scr = nullptr;
+  const qd_status st = noalloc_scratch(dev, &scr);
+  if (st != QD_OK) return st;
+  static_assert(kScratchDoubles >= 4, "k_stats writes four results");
+  return stats_into(h, qd_offset, (hipStream_t)stream, scr, out);
 }
 
 qd_status qd_archive_layout(const qd_archive* h, qd_layout* out) {

@@ -32,7 +32,7 @@ KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
 
 # Every symbol include/qd.h declares.
 EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_generations",
-           "qd_archive_stats",
+           "qd_archive_stats", "qd_archive_stats_noalloc",
            "qd_archive_layout", "qd_normal_table", "qd_sample_normals", "qd_set_kernel_timing",
            "qd_kernel_times",
            "qd_check_fast_arith", "qd_archive_destroy", "qd_status_str"]
@@ -93,6 +93,7 @@ def lib():
         L.qd_generation.argtypes = [P, C.c_uint32, P]
         L.qd_generations.argtypes = [P, C.c_uint32, C.c_uint32, P]
         L.qd_archive_stats.argtypes = [P, C.c_double, P, C.POINTER(QdStats)]
+        L.qd_archive_stats_noalloc.argtypes = [P, C.c_double, P, C.POINTER(QdStats)]
         L.qd_archive_layout.argtypes = [P, C.POINTER(QdLayout)]
         L.qd_sample_normals.argtypes = [P, P, P, C.c_uint64, P]
         L.qd_normal_table.argtypes = [C.POINTER(C.c_float)]
@@ -237,10 +238,13 @@ class Archive:
         self.stream.synchronize()
         return d_z.cpu().numpy()
 
-    def stats(self, offset: float = 0.0) -> dict:
+    def stats(self, offset: float = 0.0, noalloc: bool = False) -> dict:
+        """QD-score, coverage, best objective and flags (qd_archive_stats, or
+        with noalloc=True qd_archive_stats_noalloc)."""
         out = QdStats()
-        _check(lib().qd_archive_stats(self._h, offset, C.c_void_p(_stream_handle(self.stream)),
-                                      C.byref(out)), "qd_archive_stats")
+        fn = lib().qd_archive_stats_noalloc if noalloc else lib().qd_archive_stats
+        _check(fn(self._h, offset, C.c_void_p(_stream_handle(self.stream)), C.byref(out)),
+               "qd_archive_stats_noalloc" if noalloc else "qd_archive_stats")
         return dict(qd_score=out.qd_score, coverage=out.coverage, best=out.best_fitness,
                     num_occupied=out.num_occupied, flags=out.flags)
 

@@ -160,6 +160,9 @@ def test_workspace_checks_happen_before_gpu_work(lib):
     assert lib.qd_sample_normals(fake, None, buf, 4, None) == Q.QD_ERR_INVALID_ARG
     assert lib.qd_sample_normals(fake, buf, C.c_void_p((1 << 41) + 2), 4, None) == Q.QD_ERR_INVALID_ARG
     assert lib.qd_sample_normals(fake, None, None, 0, None) == Q.QD_OK
+    st_out = Q.QdStats()
+    assert lib.qd_archive_stats_noalloc(None, 0.0, None, C.byref(st_out)) == Q.QD_ERR_INVALID_ARG
+    assert lib.qd_archive_stats_noalloc(fake, 0.0, None, None) == Q.QD_ERR_INVALID_ARG
     assert lib.qd_archive_destroy(None) == Q.QD_OK
     assert Q.status_str(Q.QD_ERR_WORKSPACE_TOO_SMALL) == "workspace too small"
 
