@@ -105,7 +105,12 @@ typedef struct {
   uint64_t seed;          /* key of every Philox4x32-10 stream                    */
 } qd_config;
 
-/* Workspace buffers, in layout order.  Offsets/sizes are in bytes. */
+/* Workspace buffers, in layout order.  Offsets/sizes are in bytes.  The
+ * archive's state between generations is ARCHIVE_KEY .. ARCHIVE_GENO,
+ * OCC_LIST and COUNTERS: copied out together with the next generation index
+ * and written into the workspace of a fresh archive of the same
+ * configuration (after its qd_archive_init), they let the run continue bit
+ * for bit (checkpoint and resume). */
 enum {
   QD_BUF_ARCHIVE_KEY = 0,  /* u64 [C]   0 = empty; else (order(f) << 32) | 0xFFFFFFFF */
   QD_BUF_ARCHIVE_FIT,      /* f32 [C]   objective of the elite (NaN when empty)       */
