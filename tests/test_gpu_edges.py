@@ -243,3 +243,66 @@ def test_checkpoint_and_resume(name, kw):
     for k in ("parents", "fit", "desc", "cell", "won"):
         np.testing.assert_array_equal(lf[k], lw[k], err_msg=k)
     assert fresh.stats()["qd_score"] == whole.stats()["qd_score"]
+
+
+CHILD = r"""
+import sys, numpy as np
+sys.path.insert(0, sys.argv[1])
+from paper_2202_01258_amd import qd, workloads as W
+out = {}
+for k, (name, kw) in enumerate([("rastrigin_proj_cvt_b65536", {}), ("mlp64_cvt_b8192", {})]):
+    a = qd.Archive(W.workload(name, **kw))
+    a.generations(1, 2)
+    s, b = a.snapshot(), a.last_batch()
+    for f in ("key", "fit", "desc", "geno", "slot", "occ_list"):
+        out[f"{k}_{f}"] = s[f]
+    for f in ("parents", "fit", "desc", "cell", "won"):
+        out[f"{k}_b{f}"] = b[f]
+import time, torch
+a = qd.Archive(W.workload("rastrigin_proj_cvt_b65536"))
+a.generations(1, 5)
+torch.cuda.synchronize()
+t0 = time.perf_counter()
+a.generations(6, 20)
+torch.cuda.synchronize()
+out["seconds_20"] = np.float64(time.perf_counter() - t0)
+np.savez(sys.argv[2], **out)
+print("child done", flush=True)
+"""
+
+
+def test_generations_repeat_in_a_fresh_process_on_few_cus(tmp_path):
+    """The benchmark configuration and the 27-64-64-8 policy configuration,
+    two generations each, in a fresh process whose queues may use compute
+    units 0 .. 15 only (HSA_CU_MASK), against this process on the whole
+    chip: the same archives and batches, bit for bit."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    dst = str(tmp_path / "child.npz")
+    say("fresh process on 16 compute units: configuration 3 and the 27-64-64-8 policies")
+    env = dict(os.environ, HSA_CU_MASK="0:0-15")
+    r = subprocess.run([sys.executable, "-c", CHILD, root, dst], env=env, capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    got = np.load(dst)
+    for k, (name, kw) in enumerate([("rastrigin_proj_cvt_b65536", {}), ("mlp64_cvt_b8192", {})]):
+        a = qd().Archive(W.workload(name, **kw))
+        a.generations(1, 2)
+        s, b = a.snapshot(), a.last_batch()
+        for f in ("key", "fit", "desc", "geno", "slot", "occ_list"):
+            np.testing.assert_array_equal(got[f"{k}_{f}"], s[f], err_msg=f"{name} {f}")
+        for f in ("parents", "fit", "desc", "cell", "won"):
+            np.testing.assert_array_equal(got[f"{k}_b{f}"], b[f], err_msg=f"{name} batch {f}")
+    # the mask took effect: the same 20 generations are several times slower there
+    import time
+    a = qd().Archive(W.workload("rastrigin_proj_cvt_b65536"))
+    a.generations(1, 5)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    a.generations(6, 20)
+    torch.cuda.synchronize()
+    here = time.perf_counter() - t0
+    say(f"20 generations: {float(got['seconds_20']) * 1e3:.2f} ms on 16 CUs, {here * 1e3:.2f} ms here")
+    assert float(got["seconds_20"]) > 4.0 * here
