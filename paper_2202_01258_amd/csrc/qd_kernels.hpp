@@ -110,18 +110,23 @@ __device__ __forceinline__ Pair select_pair(const Params& p, uint32_t g, int j, 
 
 // The same pair, rebuilt after the generation from what the offspring
 // recorded (cells and banks) -- independent of the archive's current state.
-__device__ __forceinline__ Pair recorded_pair(const Params& p, uint32_t g, int j,
-                                              const Tables& tb) {
+__device__ __forceinline__ Pair pair_from_record(const Params& p, uint32_t g, int j, int c1, int c2,
+                                                 uint32_t banks, const Tables& tb) {
   const uint4 x = philox(0u, (uint32_t)j, g, kTagSelect, p.key);
   Pair q;
-  q.c1 = p.off_par[2 * j];
-  q.c2 = p.off_par[2 * j + 1];
-  q.banks = p.off_bank[j];
+  q.c1 = c1;
+  q.c2 = c2;
+  q.banks = banks;
   q.tb = tb;
   q.lambda = p.line_sigma * normal(x.z, tb);
   q.row1 = geno_row(p, q.banks & 1u, q.c1);
   q.row2 = geno_row(p, (q.banks >> 1) & 1u, q.c2);
   return q;
+}
+
+__device__ __forceinline__ Pair recorded_pair(const Params& p, uint32_t g, int j,
+                                              const Tables& tb) {
+  return pair_from_record(p, g, j, p.off_par[2 * j], p.off_par[2 * j + 1], p.off_bank[j], tb);
 }
 
 // Genes base..base+3 of offspring j (base a multiple of 4).  GEN0: the random
@@ -889,16 +894,6 @@ __device__ __forceinline__ bool stage_keys(const Params& p, int first, uint64_t*
   return __syncthreads_or(won) != 0;
 }
 
-// After a wave has written its genotypes: lane t < kRegenCellsPerWave
-// finishes the wave's cell t if it won.
-__device__ __forceinline__ void finish_wave_cells(const Params& p, int wfirst, const uint64_t* w_key,
-                                                  int lane) {
-  if (lane < kRegenCellsPerWave) {
-    const uint64_t key = w_key[lane];
-    if (names_offspring(key)) finish_winner(p, wfirst + lane, p.nb - 1 - (int)(uint32_t)key, key);
-  }
-}
-
 // Workgroups 0 .. ceil(C / cells) - 1 take cells; one more compacts.
 inline unsigned regen_blocks(int C, int cells) { return (unsigned)((C + cells - 1) / cells) + 1u; }
 
@@ -913,25 +908,55 @@ __global__ __launch_bounds__(256) void k_regen(const Params p, uint32_t g) {
   __shared__ uint64_t s_key[kRegenCells];
   __shared__ float4 s_ntab[kNormalRows];
   if (!stage_keys<kRegenCells>(p, first, s_key)) return;
+  const int wfirst = first + wave * kRegenCellsPerWave;
+  const uint64_t* w_key = s_key + wave * kRegenCellsPerWave;
+  // lane t < kRegenCellsPerWave reads what its cell's winner recorded (test
+  // functions have two descriptor components), in flight with the table's loads
+  const uint64_t my_key = lane < kRegenCellsPerWave ? w_key[lane] : 0ull;
+  const bool my_won = names_offspring(my_key);
+  const int my_j = p.nb - 1 - (int)(uint32_t)my_key;
+  int par1 = 0, par2 = 0, banks = 0, slot = 0;
+  float fit = 0.0f, desc[2] = {0.0f, 0.0f};
+  if (my_won) {
+    if (!GEN0) {
+      par1 = p.off_par[2 * my_j];
+      par2 = p.off_par[2 * my_j + 1];
+      banks = p.off_bank[my_j];
+    }
+    slot = (int)p.arch_slot[wfirst + lane];
+    fit = p.off_fit[my_j];
+    desc[0] = p.off_desc[2 * (size_t)my_j];
+    desc[1] = p.off_desc[2 * (size_t)my_j + 1];
+  }
   if (!GEN0) {
     stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, 256);
     __syncthreads();
   }
   const Tables tb{s_ntab};
-  const int wfirst = first + wave * kRegenCellsPerWave;
-  const uint64_t* w_key = s_key + wave * kRegenCellsPerWave;
   for (int t = 0; t < kRegenCellsPerWave; ++t) {
     const uint64_t key = w_key[t];
     if (!names_offspring(key)) continue;
     const int c = wfirst + t;
     const int j = p.nb - 1 - (int)(uint32_t)key;
     Pair q{nullptr, nullptr, 0.0f, -1, -1, 0u};
-    if (!GEN0) q = recorded_pair(p, g, j, tb);
-    float* dst = geno_row(p, p.arch_slot[c] ^ 1u, c);
+    if (!GEN0)
+      q = pair_from_record(p, g, j, __builtin_amdgcn_readlane(par1, t),
+                           __builtin_amdgcn_readlane(par2, t),
+                           (uint32_t)__builtin_amdgcn_readlane(banks, t), tb);
+    float* dst = geno_row(p, (uint32_t)__builtin_amdgcn_readlane(slot, t) ^ 1u, c);
     for (int base = 4 * lane; base < p.n; base += 256)
       *reinterpret_cast<float4*>(dst + base) = make_genes<GEN0>(p, q, g, j, base);
   }
-  finish_wave_cells(p, wfirst, w_key, lane);
+  // then lane t finishes its cell: objective, descriptor, bank, incumbent key
+  if (my_won) {
+    const int c = wfirst + lane;
+    p.arch_fit[c] = fit;
+    p.arch_desc[2 * (size_t)c] = desc[0];
+    p.arch_desc[2 * (size_t)c + 1] = desc[1];
+    p.off_won[my_j] = 1;
+    p.arch_slot[c] = (uint32_t)slot ^ 1u;
+    p.arch_key[c] = my_key | 0xffffffffull;
+  }
 }
 
 // ---------------------------------------------------------------------------
