@@ -158,7 +158,8 @@ def kernel_name_of(w: dict) -> tuple[str, str]:
     """(timing key, profiler name) of the dominant kernel of a workload."""
     if w["task"] == 3:
         return "rollout", f"k_rollout<{w['hid']}, false, false>"
-    return "vary_eval", f"k_vary_eval<{w['task']}, false, false>"
+    from paper_2202_01258_amd import qd
+    return "vary_eval", f"k_vary_eval<{w['task']}, false, false, {qd.offspring_per_wave(w['batch'])}>"
 
 
 def measure(name: str, w: dict, steps: int, warmup: int, kernel_timing: bool = True) -> dict:

@@ -2,7 +2,8 @@
 //
 // Pipeline of one generation (Algorithm 1 after the first iteration; the
 // first iteration runs the same kernels with the random-init genotype):
-//   k_vary_eval   a wave takes 4 offspring (two at a time, one per half-wave,
+//   k_vary_eval   a wave takes 4 offspring (1 in batches of at most 2048, 2 in
+//                 batches of at most 8192; two at a time, one per half-wave,
 //                 for genotypes of at most 128 genes): draws their parents
 //                 uniformly from the filled cells (Appendix A.2), runs Iso+LineDD
 //                 (Algorithm 2) gene by gene on coalesced float4 rows of both parents with
@@ -430,17 +431,29 @@ __device__ __forceinline__ void insert_one(const Params& p, int cell, uint64_t k
 
 // ---------------------------------------------------------------------------
 // Select + vary + evaluate + cell + insert (test functions).  A wave takes
-// kOffspringPerWave consecutive offspring: lanes 0..3 draw their parents
-// together, then the whole wave runs each offspring's genes in turn (lane l
-// owns genes 256c + 4l .. 256c + 4l + 3 of every chunk c, i.e. gene groups
-// q = g/4 with q mod 64 = l; its partial sums run in ascending gene order and
-// the wave folds them pairwise, h = 32 .. 1); finally lanes 0..3 find their
-// offspring's cell and insert its key.
+// OPW consecutive offspring: lanes 0 .. OPW-1 draw their parents together,
+// then the whole wave runs each offspring's genes in turn (lane l owns genes
+// 256c + 4l .. 256c + 4l + 3 of every chunk c, i.e. gene groups q = g/4 with
+// q mod 64 = l; its partial sums run in ascending gene order and the wave
+// folds them pairwise, h = 32 .. 1); finally lanes 0 .. OPW-1 find their
+// offspring's cell and insert its key.  Large batches take four offspring per
+// wave (the per-wave set-up -- sampler table, selection -- spread over more
+// work); small ones fewer, since there a generation is a chain of dependent
+// memory round trips and more waves in flight shorten it: one offspring per
+// wave up to kOneOffspringBatch, two up to kTwoOffspringBatch.  Every choice
+// gives the same bits (each offspring's arithmetic does not depend on it).
 // ---------------------------------------------------------------------------
-constexpr int kOffspringPerWave = 4;
+constexpr int kOffspringPerWave = 4;             // the most a wave takes
+constexpr int kOneOffspringBatch = 2048;
+constexpr int kTwoOffspringBatch = 8192;
 
-template <int TASK, bool GEN0, bool KEEP>
+inline int offspring_per_wave(int nb) {
+  return nb <= kOneOffspringBatch ? 1 : (nb <= kTwoOffspringBatch ? 2 : kOffspringPerWave);
+}
+
+template <int TASK, bool GEN0, bool KEEP, int OPW>
 __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
+  static_assert(OPW == 1 || OPW == 2 || OPW == kOffspringPerWave, "one, two or four offspring");
   __shared__ float4 s_ntab[kNormalRows];
   if (!GEN0) {
     stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, 256);
@@ -448,9 +461,9 @@ __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   }
   const Tables tb{s_ntab};
   const int lane = threadIdx.x & 63;
-  const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kOffspringPerWave;
+  const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * OPW;
   if (j0 >= p.nb) return;
-  const int nmine = p.nb - j0 < kOffspringPerWave ? p.nb - j0 : kOffspringPerWave;
+  const int nmine = p.nb - j0 < OPW ? p.nb - j0 : OPW;
   const bool mine = lane < nmine;          // lane i speaks for offspring j0 + i
 
   Pair sel{nullptr, nullptr, 0.0f, -1, -1, 0u};

@@ -304,23 +304,31 @@ unsigned blocks_for(uint64_t items, unsigned per_block) {
   return (unsigned)((items + per_block - 1) / per_block);
 }
 
+template <int TASK, bool GEN0, int OPW>
+void launch_vary_eval_as(const Go& go, dim3 grid, const qd::Params& p, uint32_t g, bool keep) {
+  if (keep) go(qd::k_vary_eval<TASK, GEN0, true, OPW>, grid, dim3(256), p, g);
+  else go(qd::k_vary_eval<TASK, GEN0, false, OPW>, grid, dim3(256), p, g);
+}
+
+template <int TASK, bool GEN0>
+void launch_vary_eval_task(const Go& go, const qd::Params& p, uint32_t g, bool keep) {
+  const int opw = qd::offspring_per_wave(p.nb);
+  const dim3 grid(blocks_for((uint64_t)p.nb, 4u * (unsigned)opw));
+  if (opw == 1) launch_vary_eval_as<TASK, GEN0, 1>(go, grid, p, g, keep);
+  else if (opw == 2) launch_vary_eval_as<TASK, GEN0, 2>(go, grid, p, g, keep);
+  else launch_vary_eval_as<TASK, GEN0, qd::kOffspringPerWave>(go, grid, p, g, keep);
+}
+
 template <bool GEN0>
 void launch_vary_eval(qd_archive* h, hipStream_t s, uint32_t g) {
   const qd::Params& p = h->p;
-  const dim3 grid(blocks_for((uint64_t)p.nb, 4 * qd::kOffspringPerWave)), block(256);
   const Go go{h, s, QD_K_VARY_EVAL};
   const bool keep = h->cfg.keep_offspring != 0;
-#define QD_VE(TASK)                                                            \
-  do {                                                                         \
-    if (keep) go(qd::k_vary_eval<TASK, GEN0, true>, grid, block, p, g);        \
-    else go(qd::k_vary_eval<TASK, GEN0, false>, grid, block, p, g);           \
-  } while (0)
   switch (p.task) {
-    case qd::kTaskRastrigin: QD_VE(qd::kTaskRastrigin); break;
-    case qd::kTaskSphere: QD_VE(qd::kTaskSphere); break;
-    default: QD_VE(qd::kTaskProj); break;
+    case qd::kTaskRastrigin: launch_vary_eval_task<qd::kTaskRastrigin, GEN0>(go, p, g, keep); break;
+    case qd::kTaskSphere: launch_vary_eval_task<qd::kTaskSphere, GEN0>(go, p, g, keep); break;
+    default: launch_vary_eval_task<qd::kTaskProj, GEN0>(go, p, g, keep); break;
   }
-#undef QD_VE
 }
 
 void launch_insert(qd_archive* h, hipStream_t s) {

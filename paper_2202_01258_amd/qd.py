@@ -30,6 +30,17 @@ QD_OK, QD_ERR_INVALID_ARG, QD_ERR_WORKSPACE_TOO_SMALL, QD_ERR_EMPTY_ARCHIVE, \
 (K_VARY_EVAL, K_ROLLOUT, K_INSERT, K_REGEN, K_SETUP, NUM_KERNELS) = range(6)
 KERNEL_NAMES = ["vary_eval", "rollout", "insert", "regen", "setup"]
 
+# Offspring per wave of the test-function generation kernel (the library's
+# choice by batch size; the same constants as in csrc/qd_kernels.hpp).  It
+# names the kernel instance a profile refers to; results do not depend on it.
+OFFSPRING_PER_WAVE, ONE_OFFSPRING_BATCH, TWO_OFFSPRING_BATCH = 4, 2048, 8192
+
+
+def offspring_per_wave(nb: int) -> int:
+    if nb <= ONE_OFFSPRING_BATCH:
+        return 1
+    return 2 if nb <= TWO_OFFSPRING_BATCH else OFFSPRING_PER_WAVE
+
 # Every symbol include/qd.h declares.
 EXPORTS = ["qd_layout_query", "qd_archive_init", "qd_generation", "qd_generations",
            "qd_archive_stats", "qd_archive_stats_noalloc",

@@ -41,7 +41,8 @@ BATCHES = sorted(set(list(range(1, 130)) + [255, 256, 257, 600, 1000, 1023, 1024
 
 
 def test_constants_found():
-    for name in ("kOffspringPerWave", "kInsertLdsOffspring", "kCvtLdsCells", "kRegenCellsPerWave",
+    for name in ("kOffspringPerWave", "kOneOffspringBatch", "kTwoOffspringBatch",
+                 "kInsertLdsOffspring", "kCvtLdsCells", "kRegenCellsPerWave",
                  "kRegenCells", "kRegenCellsMlp", "kInsertBlock", "kInsertSlots"):
         assert name in K, name
 
@@ -84,12 +85,31 @@ def test_lds_cvt_insertion_lanes(nb):
     np.testing.assert_array_equal(taken, 1)
 
 
+def offspring_per_wave(nb):
+    """The library's choice (offspring_per_wave in qd_kernels.hpp)."""
+    if nb <= K["kOneOffspringBatch"]:
+        return 1
+    return 2 if nb <= K["kTwoOffspringBatch"] else K["kOffspringPerWave"]
+
+
+def test_offspring_per_wave_choice():
+    """Four per wave in large batches, fewer in small ones; the selection and
+    cell-search lanes (0 .. P-1, rows of 16 lanes for four offspring) hold P."""
+    assert K["kOffspringPerWave"] == 4
+    assert 0 < K["kOneOffspringBatch"] < K["kTwoOffspringBatch"]
+    assert [offspring_per_wave(nb) for nb in (1, 2048, 2049, 8192, 8193, 65536)] == [1, 1, 2, 2, 4, 4]
+    from paper_2202_01258_amd import qd     # the binding names kernel instances by it
+    assert (qd.OFFSPRING_PER_WAVE, qd.ONE_OFFSPRING_BATCH, qd.TWO_OFFSPRING_BATCH) == (
+        K["kOffspringPerWave"], K["kOneOffspringBatch"], K["kTwoOffspringBatch"])
+    assert all(qd.offspring_per_wave(nb) == offspring_per_wave(nb) for nb in BATCHES)
+
+
 @pytest.mark.parametrize("nb", BATCHES)
 def test_vary_eval_offspring_lanes(nb):
     """k_vary_eval: grid ceil(nb / (4 P)) x 256; wave w of workgroup b takes
     offspring j0 = (4 b + w) P .. j0 + nmine - 1, lane i < nmine speaking for
     j0 + i."""
-    P = K["kOffspringPerWave"]
+    P = offspring_per_wave(nb)
     blocks = ceil_div(nb, 4 * P)
     taken = np.zeros(nb, np.int64)
     for b in range(blocks):

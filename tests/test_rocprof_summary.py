@@ -5,7 +5,7 @@ import os
 
 from paper_2202_01258_amd import rocprof_summary as R
 
-VARY = "k_vary_eval<2, false, false>"
+VARY = "k_vary_eval<2, false, false, 4>"
 ROLL = "k_rollout<64, false, false>"
 
 
