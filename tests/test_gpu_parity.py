@@ -201,6 +201,11 @@ def test_generations_driven_bit_exact(name):
     # every early generation (regeneration and compaction at full load)
     ("rastrigin_grid_b128", dict(batch=4096, init_lo=-5.12, init_hi=5.12, seed=2), 40),
     ("sphere_grid_b16384", dict(batch=4096, init_lo=-5.12, init_hi=5.12, seed=3), 10),
+    # the generation kernel's offspring-per-wave thresholds (one up to 2048, two
+    # up to 8192, four above), each side, with ragged last waves
+    ("rastrigin_grid_b128", dict(batch=2049, init_lo=-5.12, init_hi=5.12, seed=4), 20),
+    ("sphere_grid_b16384", dict(batch=8192, init_lo=-5.12, init_hi=5.12, seed=6), 10),
+    ("rastrigin_proj_cvt_b65536", dict(batch=8193, n=300, seed=5), 3),
 ])
 def test_end_to_end_qd_score(name, kw, G):
     w = W.workload(name, **kw)
