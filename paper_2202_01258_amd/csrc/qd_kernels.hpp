@@ -455,25 +455,42 @@ template <int TASK, bool GEN0, bool KEEP, int OPW>
 __global__ __launch_bounds__(256) void k_vary_eval(const Params p, uint32_t g) {
   static_assert(OPW == 1 || OPW == 2 || OPW == kOffspringPerWave, "one, two or four offspring");
   __shared__ float4 s_ntab[kNormalRows];
-  if (!GEN0) {
-    stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, 256);
-    __syncthreads();
-  }
   const Tables tb{s_ntab};
   const int lane = threadIdx.x & 63;
   const int j0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * OPW;
-  if (j0 >= p.nb) return;
   const int nmine = p.nb - j0 < OPW ? p.nb - j0 : OPW;
   const bool mine = lane < nmine;          // lane i speaks for offspring j0 + i
 
+  // The parents' cells and banks (Appendix A.2) are read while the sampler
+  // table is being staged: the chain filled-cell count -> list entry -> bank
+  // runs beside the table's loads; the line coefficient, which needs the
+  // table, comes after the barrier.
   Pair sel{nullptr, nullptr, 0.0f, -1, -1, 0u};
+  int nocc = 0;
+  uint32_t sel_z = 0u;
   if (!GEN0) {
-    const int nocc = p.counters[0];
+    nocc = p.counters[0];
+    if (mine && nocc > 0) {
+      const uint4 x = philox(0u, (uint32_t)(j0 + lane), g, kTagSelect, p.key);
+      sel.c1 = pick(p.occ_list, x.x, nocc);
+      sel.c2 = pick(p.occ_list, x.y, nocc);
+      sel.banks = p.arch_slot[sel.c1] | (p.arch_slot[sel.c2] << 1);
+      sel_z = x.z;
+    }
+    stage_normal_table(s_ntab, p.ntab, (int)threadIdx.x, 256);
+    __syncthreads();
+  }
+  if (j0 >= p.nb) return;
+  if (!GEN0) {
     if (nocc <= 0) {
       if (mine) record_empty_archive(p, j0 + lane);
       return;
     }
-    if (mine) sel = select_pair(p, g, j0 + lane, nocc, tb);
+    if (mine) {
+      sel.lambda = p.line_sigma * normal(sel_z, tb);
+      sel.row1 = geno_row(p, sel.banks & 1u, sel.c1);
+      sel.row2 = geno_row(p, (sel.banks >> 1) & 1u, sel.c2);
+    }
   }
 
   const int n = p.n;
