@@ -8,7 +8,7 @@
 // instruction per SIMD at the published 2.4 GHz clock, for
 //   * single instruction forms at 8 waves per SIMD (8 chains per wave);
 //   * a 1:1 mix of an fma and a v_max_f32 (two instructions per issue slot);
-//   * fma and DPP-broadcast fma on 8 and on 4 chains at 1, 2, 4 and 8 waves
+//   * fma and DPP-broadcast fma on 8 and on 4 chains at 1, 2, 3, 4 and 8 waves
 //     per SIMD;
 //   * Philox4x32-10 with 64-bit multiply-adds against low/high multiplies.
 #include <hip/hip_runtime.h>
@@ -184,11 +184,11 @@ bool ok(hipError_t e) {
 
 // Best of three launches, in ms.
 bool time_kernel(kern_t k, int blocks, int iters, float* out, hipEvent_t e0, hipEvent_t e1,
-                 float* best) {
+                 float* best, size_t lds = 0) {
   *best = 1e30f;
   for (int r = 0; r < 3; ++r) {
     if (!ok(hipEventRecord(e0, 0))) return false;
-    hipLaunchKernelGGL(k, dim3(blocks), dim3(kThreads), 0, 0, out, iters);
+    hipLaunchKernelGGL(k, dim3(blocks), dim3(kThreads), lds, 0, out, iters);
     if (!ok(hipGetLastError()) || !ok(hipEventRecord(e1, 0)) || !ok(hipEventSynchronize(e1)))
       return false;
     float ms = 0.0f;
@@ -228,16 +228,32 @@ int main() {
     const double per_simd = (double)kMaxBlocks * kThreads / 64.0 / 1024.0 * iters * c.per_iter;
     std::printf("%-30s %8.3f ms  %5.2f cycles\n", c.name, ms, ms * 1e-3 * 2.4e9 / per_simd);
   }
-  std::printf("# the same per SIMD at 1, 2, 4, 8 waves per SIMD (256 x waves workgroups)\n");
+  // Waves per SIMD pinned by LDS: a workgroup (4 waves) takes 160 KB / (w + 1)
+  // < bytes <= 160 KB / w of dynamic LDS, so w workgroups fit a CU and w + 1 do
+  // not; 2048 workgroups run in rounds at that occupancy.  One wave per SIMD:
+  // 256 workgroups, one per CU, in a single round.
+  int lds_per_cu = 0;
+  if (!ok(hipDeviceGetAttribute(&lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, 0)))
+    return 1;
+  std::printf("# the same per SIMD at 1, 2, 3, 4, 8 waves per SIMD (LDS per CU %d bytes)\n", lds_per_cu);
   const Case chains[] = {{"v_fma_f32, 8 chains", k_fma, 16},
                          {"v_fmac_f32_dpp, 8 chains", k_dpp, 16},
                          {"v_fma_f32, 4 chains", k_fma4, 16},
                          {"v_fmac_f32_dpp, 4 chains", k_dpp4, 16}};
+  const int chain_iters = 20000;
   for (const Case& c : chains) {
-    for (int wps = 1; wps <= 8; wps *= 2) {
+    for (int wps : {1, 2, 3, 4, 8}) {
+      const int blocks = wps == 1 ? 256 : kMaxBlocks;
+      const size_t lds = wps == 1 ? 0 : (size_t)(lds_per_cu / wps) & ~(size_t)1023;
+      if (wps > 1 && (lds * (size_t)(wps + 1) <= (size_t)lds_per_cu ||
+                      hipFuncSetAttribute((const void*)c.k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                          (int)lds) != hipSuccess)) {
+        std::printf("%-30s %d waves/SIMD: LDS cannot pin it\n", c.name, wps);
+        continue;
+      }
       float ms;
-      if (!time_kernel(c.k, 256 * wps, iters, out, e0, e1, &ms)) return 2;
-      const double per_simd = (double)wps * iters * c.per_iter;
+      if (!time_kernel(c.k, blocks, chain_iters, out, e0, e1, &ms, lds)) return 2;
+      const double per_simd = (double)blocks * 4.0 / 1024.0 * chain_iters * c.per_iter;
       std::printf("%-30s %d waves/SIMD %8.3f ms  %5.2f cycles\n", c.name, wps, ms,
                   ms * 1e-3 * 2.4e9 / per_simd);
     }
