@@ -332,8 +332,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the method shards as described in DESIGN.md, but only one GPU is used here)",
-              file=sys.stderr)
+              "(this path runs and is measured on a single GPU)", file=sys.stderr)
         sys.exit(2)
 
     import torch
