@@ -55,7 +55,7 @@ def log(msg: str):
 
 
 def algorithmic_bytes(w: dict, n: int) -> dict:
-    """Bytes each offspring must move at least (byte model).
+    """Bytes each offspring must move at least (the byte model: every parent row read from HBM).
 
     vary_eval: both parent rows (8n), objective and descriptor (4 + 4D), two
     parent indices (8), won flag (1).  Whole generation adds the cell index
