@@ -352,6 +352,8 @@ MLP_SMALL = {
                             dict(batch=64, T=60, death_mode=2, death_below=-0.05)),
     "mlp128_death_truncate": ("mlp128_cvt_b65536",
                               dict(batch=24, T=40, C=500, death_mode=1, death_below=-0.03)),
+    "mlp128_death_discard": ("mlp128_cvt_b65536",
+                             dict(batch=24, T=40, C=500, death_mode=2, death_below=-0.03)),
     # a batch that is not a multiple of the 16 offspring an LDS-CVT insertion
     # workgroup takes, on a CVT smaller than one centroid per lane
     "mlp64_odd_batch_small_cvt": ("mlp64_cvt_b8192", dict(batch=37, T=12, C=13)),
