@@ -185,7 +185,12 @@ def masked_stream(n_cus):
 
 @pytest.mark.parametrize("name,kw", [("rastrigin_proj_cvt_b65536", {}),
                                      ("mlp64_cvt_b8192", {}),
-                                     ("rastrigin_proj_cvt_b65536", dict(init_mode=1))])
+                                     ("rastrigin_proj_cvt_b65536", dict(init_mode=1)),
+                                     # one and two offspring per wave, whole-box first batch
+                                     ("rastrigin_grid_b128", dict(batch=2000, init_lo=-5.12,
+                                                                  init_hi=5.12, seed=8)),
+                                     ("sphere_grid_b16384", dict(batch=6000, init_lo=-5.12,
+                                                                 init_hi=5.12, seed=9))])
 def test_generations_repeat_on_a_few_compute_units(name, kw):
     w = W.workload(name, **kw)
     say(f"repeatability on 16 compute units: {name} {kw}")
